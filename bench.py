@@ -1,0 +1,256 @@
+"""Benchmark one streaming step of chunk-streamed attention on one MI355X.
+
+A step is the whole hot path for one batch: frt_stream_attn_step (chunk
+preparation + attention) followed by frt_kv_append, or for the decode
+workload frt_decode_attn (split + combine) followed by a one-token append.
+Inputs are seeded synthetic bf16 tensors already resident in HBM; the ring is
+pre-filled through the library's own append so the measured steps see a
+wrapped ring.
+
+Prints one JSON line. `value` is attention TFLOP/s per step (algorithmic
+flops: 4*d per visible (query, key) pair, no credit for masked or padded
+work) or, for decode, HBM GB/s per step (each visible K/V byte once plus
+q/out). `roofline` reports the dominant kernel against MI355X's published
+peaks, timed with HIP events on the kernel's stream inside the timed loop.
+`cpu_baseline` times the fp64 oracle on a bounded sample of the same step.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from workloads import WORKLOADS, make_case, MASK_BLOCK_CAUSAL, MASK_CAUSAL  # noqa: E402
+
+METRIC = "attention TFLOP/s + % bf16 MFMA peak per streaming step; decode HBM GB/s"
+PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA (published 2.5 PFLOP/s)
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published 8 TB/s)
+
+
+def visible_counts(wl, L: int):
+    """Number of keys each query i of a stream holding L tokens attends to."""
+    i = np.arange(wl.n, dtype=np.int64)
+    p = L + i
+    if wl.mask.kind == MASK_BLOCK_CAUSAL:
+        bp = p // wl.mask.block
+        lo = (bp - wl.mask.window) * wl.mask.block if wl.mask.window else np.zeros_like(p)
+        hi = (bp + 1) * wl.mask.block - 1
+    else:
+        lo = p - wl.mask.window + 1 if wl.mask.window else np.zeros_like(p)
+        hi = p
+    present_lo = max(0, L - wl.C)
+    present_hi = L + wl.n - 1
+    lo = np.maximum(lo, present_lo)
+    hi = np.minimum(hi, present_hi)
+    return np.maximum(hi - lo + 1, 0)
+
+
+def step_work(wl, lengths):
+    """(attention flops, minimum HBM bytes) of one step for per-stream lengths."""
+    flops = 0
+    kv_bytes = 0
+    for L in lengths:
+        cnt = visible_counts(wl, int(L))
+        flops += int(cnt.sum()) * 4 * wl.d * wl.Hq
+        # distinct keys read by the stream: union over queries
+        kv_bytes += int(cnt.max()) * wl.Hkv * wl.d * 2 * 2
+    qo_bytes = 2 * wl.B * wl.n * wl.Hq * wl.d * 2
+    return flops, kv_bytes + qo_bytes
+
+
+def cpu_baseline(wl, case, budget_rows: int):
+    """Time the fp64 oracle on a bounded sample of the measured step."""
+    import oracle
+    try:
+        import threadpoolctl
+        threads = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()) or 1
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    oring = oracle.new_ring(wl.B, wl.Hkv, wl.C, wl.d)
+    for k, v in case.prior_steps:
+        oring = oracle.kv_append(oring, k, v, wl.rope)
+    for b, (k, v) in enumerate(case.prior_fills):
+        for s in range(0, k.shape[1], wl.C):
+            e = min(k.shape[1], s + wl.C)
+            oring = oracle.kv_append(oring, k[:, s:e], v[:, s:e], wl.rope, streams=[b])
+    rows = np.arange(min(wl.n, budget_rows), dtype=np.int64)
+    t0 = time.perf_counter()
+    oracle.stream_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask, rows=rows)
+    dt = time.perf_counter() - t0
+    flops = 0
+    for L in case.prior_lengths:
+        flops += int(visible_counts(wl, int(L))[rows].sum()) * 4 * wl.d * wl.Hq
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": "%d of %d query tokens per stream, all %d heads (%.2f GFLOP fp64 in %.1f s)"
+                      % (len(rows), wl.n, wl.Hq, flops / 1e9, dt)}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="video_1p3b", choices=sorted(WORKLOADS))
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-rows", type=int, default=256,
+                    help="query tokens per stream in the oracle's timed sample (0 = skip)")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the chunk step runs on one MI355X and nothing "
+              "crosses GPUs in this build (requested --gpus %d)" % args.gpus, file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2607_18171_amd as frt
+
+    wl = WORKLOADS[args.workload]
+    case = make_case(wl, args.seed)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+
+    def to_dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(
+            torch.bfloat16).to(dev)
+
+    total_steps = args.warmup + args.steps
+    max_tokens = int(case.prior_lengths.max()) + (total_steps + 1) * wl.n + 1
+    rope = frt.Rope.for_tokens(wl.rope.mode, wl.rope.axis_dims, wl.rope.frame_hw, max_tokens,
+                               wl.rope.base)
+    ring = frt.Ring(wl.B, wl.Hkv, wl.d, wl.C)
+    for k, v in case.prior_steps:
+        frt.kv_append(ring, rope, to_dev(k), to_dev(v))
+    for b, (k, v) in enumerate(case.prior_fills):
+        for s in range(0, k.shape[1], wl.C):
+            e = min(k.shape[1], s + wl.C)
+            frt.kv_append(ring.view_stream(b), rope, to_dev(k[:, s:e]), to_dev(v[:, s:e]))
+    q, kn, vn = to_dev(case.q), to_dev(case.k_new), to_dev(case.v_new)
+    out = torch.empty_like(q)
+    msk = frt.mask(wl.mask.kind, wl.mask.block, wl.mask.window)
+    decode = wl.n == 1
+    if decode:
+        ws = torch.empty(frt.decode_workspace_bytes(ring, wl.Hq), dtype=torch.uint8, device=dev)
+    else:
+        ws = torch.empty(frt.stream_attn_workspace_bytes(ring, wl.n, wl.Hq), dtype=torch.uint8,
+                         device=dev)
+    torch.cuda.synchronize()
+
+    def step():
+        if decode:
+            frt.decode_attn(ring, rope, msk, q, kn, vn, out, ws)
+        else:
+            frt.stream_attn_step(ring, rope, msk, q, kn, vn, out, ws)
+        frt.kv_append(ring, rope, kn, vn)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    lengths0 = ring.seq_len.cpu().numpy().copy()
+
+    frt.timing_reset()
+    frt.timing_enable(True)
+    stream = torch.cuda.current_stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    frt.timing_enable(False)
+    ms_total = ev0.elapsed_time(ev1)
+    ms_step = ms_total / args.steps
+
+    # algorithmic work of the timed steps (lengths advance by n per step)
+    flops = 0
+    bytes_ = 0
+    for s in range(args.steps):
+        f, by = step_work(wl, lengths0 + s * wl.n)
+        flops += f
+        bytes_ += by
+    flops_step = flops / args.steps
+    bytes_step = bytes_ / args.steps
+
+    kernels = {}
+    for name in ("chunk_prep", "chunk_attn", "decode_split", "decode_combine", "rope_append",
+                 "seq_advance"):
+        c, ms = frt.timing_query(name)
+        if c:
+            kernels[name] = {"launches": c, "avg_us": 1000.0 * ms / c}
+
+    if decode:
+        value = bytes_step / (ms_step * 1e-3) / 1e9
+        unit = "GB/s"
+        dom = kernels["decode_split"]
+        achieved = bytes_step / (dom["avg_us"] * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS, "traffic": None, "kernel": "decode_split"}
+    else:
+        value = flops_step / (ms_step * 1e-3) / 1e12
+        unit = "TFLOP/s"
+        dom = kernels["chunk_attn"]
+        achieved = flops_step / (dom["avg_us"] * 1e-6) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                "kernel": "chunk_attn"}
+
+    cpu = None
+    if args.cpu_rows > 0 and not decode:
+        cpu = cpu_baseline(wl, case, args.cpu_rows)
+    elif args.cpu_rows > 0:
+        cpu = cpu_baseline_decode(wl, case)
+
+    line = {
+        "metric": METRIC, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "streams": wl.B, "q_heads": wl.Hq, "kv_heads": wl.Hkv,
+                   "head_dim": wl.d, "chunk_tokens": wl.n, "ring_slots": wl.C,
+                   "mask": "block_causal" if wl.mask.kind == MASK_BLOCK_CAUSAL else "causal",
+                   "window": wl.mask.window, "seed": args.seed,
+                   "step_gflop": flops_step / 1e9, "step_min_mb": bytes_step / 1e6,
+                   "parallelism": "single_gpu"},
+        "kernels_us": {k: round(v["avg_us"], 2) for k, v in kernels.items()},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def cpu_baseline_decode(wl, case):
+    """Time the oracle on a bounded sample of decode streams; report GB/s of K/V visited."""
+    import oracle
+    import dataclasses
+    try:
+        import threadpoolctl
+        threads = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()) or 1
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    nb = min(wl.B, 8)
+    sub = dataclasses.replace(wl, B=nb)
+    oring = oracle.new_ring(nb, wl.Hkv, wl.C, wl.d)
+    for b in range(nb):
+        k, v = case.prior_fills[b]
+        oring = oracle.kv_append(oring, k, v, wl.rope, streams=[b])
+    t0 = time.perf_counter()
+    oracle.decode_attn(oring, case.q[:nb], case.k_new[:nb], case.v_new[:nb], wl.rope, wl.mask)
+    dt = time.perf_counter() - t0
+    _, by = step_work(sub, case.prior_lengths[:nb])
+    return {"value": by / dt / 1e9, "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+            "sample": "%d of %d streams (%.1f MB in %.2f s)" % (nb, wl.B, by / 1e6, dt)}
+
+
+if __name__ == "__main__":
+    sys.exit(main())

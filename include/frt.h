@@ -1,0 +1,231 @@
+/*
+ * frt.h - chunk-streamed attention over per-stream ring-buffer KV caches,
+ * C ABI of libfrt.so (HIP, gfx950 / MI355X).
+ *
+ * What a streaming step is. The FlashRT paper models a real-time pipeline as
+ * a task graph processed batch by batch; a node of batch j may depend on the
+ * persistent state its own instance left behind in batch j-1 (Problem
+ * Formulation: cross-batch lambda=1 edges, the example being a KV cache that
+ * batch j inherits from batch j-1; Chain-of-Program, IR design: node-level
+ * persistent-state read/write annotations; appendix "Pipeline graph"). In the
+ * autoregressive video DiTs and multimodal LLMs the paper deploys, that state
+ * is the attention KV cache, and each step's new query chunk attends to the
+ * cached keys plus its own. This library implements that step:
+ *
+ *   frt_stream_attn_step  READS the ring: out = attention(q, ring keys + own keys)
+ *   frt_decode_attn       the same for one token per stream (split-KV + combine)
+ *   frt_kv_append         WRITES the ring: stores the chunk's RoPE'd K and its V
+ *
+ * A step is frt_stream_attn_step (or frt_decode_attn) followed by
+ * frt_kv_append on the same HIP stream. Attention never sees the chunk through
+ * the ring: it reads k_new / v_new directly, so a ring whose capacity equals
+ * the visible window works even though the append then overwrites the oldest
+ * visible chunk.
+ *
+ * Arithmetic (the paper gives none; standard definitions):
+ *   score(p, k) = (rot(q_p, p) . K_k) * scale, scale = 1/sqrt(d) by default;
+ *   out_p = sum_k softmax_k(score) V_k over the keys visible to p;
+ *   rot: rotary embedding (RoFormer) on interleaved pairs (x[2i], x[2i+1]) by
+ *   angle pos * theta_i, theta_i = base^(-2i/D); 3D variant: the head
+ *   dimension is split into t/h/w slices, each rotated by that coordinate of
+ *   the token in a latent frame of H x W tokens (raster order).
+ * Stored keys are bit-exact: K = bf16(fp32(rot_fp64(k))) with fp32 cos/sin
+ * from frt_rope_table_fill and round-to-nearest-even at both roundings.
+ *
+ * Memory. Every buffer is owned by the caller; the library keeps no device
+ * allocations. Device pointers must be 16-byte aligned. bf16 is stored as
+ * 16-bit IEEE bfloat16 bit patterns. Calls are asynchronous on the given
+ * hipStream_t (NULL = the null stream) and never synchronise the host,
+ * except frt_timing_query.
+ *
+ * Errors. Every entry point validates its arguments on the host before
+ * launching anything; on failure it returns a non-zero frt_status, launches
+ * nothing and sets a thread-local message (frt_last_error). A failed launch
+ * returns FRT_ERR_HIP. Conditions the host cannot see (values of the device
+ * array seq_len) are caller contracts, stated per call.
+ */
+#ifndef FRT_H_
+#define FRT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FRT_OK = 0,
+  FRT_ERR_NULL = 1,         /* a required pointer is NULL */
+  FRT_ERR_SHAPE = 2,        /* a size is out of range or inconsistent */
+  FRT_ERR_UNSUPPORTED = 3,  /* valid but not implemented (e.g. head_dim 96) */
+  FRT_ERR_CAPACITY = 4,     /* ring capacity too small for n_new or the window */
+  FRT_ERR_ALIGN = 5,        /* capacity not a multiple of 8, or misaligned pointer */
+  FRT_ERR_WORKSPACE = 6,    /* workspace missing or smaller than required */
+  FRT_ERR_HIP = 7           /* a HIP launch/runtime call failed */
+} frt_status;
+
+enum { FRT_ROPE_NONE = 0, FRT_ROPE_1D = 1, FRT_ROPE_3D = 2 };
+enum { FRT_MASK_BLOCK_CAUSAL = 1, FRT_MASK_CAUSAL = 2 };
+
+/*
+ * Persistent per-stream state (the paper's cross-batch KV-cache state).
+ * Token t of stream b lives in slot t mod capacity. seq_len[b] counts the
+ * tokens ever appended to stream b; the tokens still held are
+ * [max(0, seq_len-capacity), seq_len).
+ *   k_ring : bf16 [num_streams][num_kv_heads][capacity][head_dim]   (row per slot)
+ *   v_ring : bf16 [num_streams][num_kv_heads][head_dim][capacity]   (slot-contiguous)
+ *   seq_len: int64 [num_streams], device memory.
+ * head_dim is 64 or 128; capacity is a positive multiple of 8. A new ring
+ * must be zero-filled with seq_len = 0 (slot contents must stay finite:
+ * never-written and masked slots are multiplied by a zero weight).
+ * The per-head size capacity*head_dim*2 bytes must be below 2^31.
+ */
+typedef struct {
+  int32_t num_streams;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t capacity;
+  void *k_ring;
+  void *v_ring;
+  int64_t *seq_len;
+} frt_ring;
+
+/*
+ * Rotary embedding description.
+ *   mode FRT_ROPE_NONE: no rotation (table unused, may be NULL).
+ *   mode FRT_ROPE_1D  : axis_dims = {D, 0, 0}, D even, D <= head_dim; pairs
+ *                       beyond D/2 are not rotated. max_pos[0] = positions held.
+ *   mode FRT_ROPE_3D  : axis_dims = {Dt, Dh, Dw}, each even, sum <= head_dim;
+ *                       frame_hw = {H, W}; token p has coordinates
+ *                       (p div HW, (p mod HW) div W, p mod W);
+ *                       max_pos = {frames, H, W} held in the table.
+ *   base: theta base (10000 in the paper's models).
+ *   table: device copy of the buffer written by frt_rope_table_fill.
+ * Contract: every token position rotated by a call lies inside max_pos
+ * (positions beyond it are clamped to the last table row, which is wrong but
+ * never reads out of bounds).
+ */
+typedef struct {
+  int32_t mode;
+  int32_t axis_dims[3];
+  int32_t frame_hw[2];
+  int32_t max_pos[3];
+  double base;
+  const float *table;
+} frt_rope;
+
+/*
+ * Visibility of key token k to query token p.
+ *   FRT_MASK_BLOCK_CAUSAL: block = tokens per block (>= 1), window = blocks
+ *       (0 = unlimited): visible iff k div block <= p div block and
+ *       (window = 0 or p div block - k div block <= window).
+ *   FRT_MASK_CAUSAL: window = keys including self (0 = unlimited):
+ *       visible iff k <= p and (window = 0 or p - k < window).
+ */
+typedef struct {
+  int32_t kind;
+  int32_t block;
+  int32_t window;
+} frt_mask;
+
+/* Bytes of the rotary table for `rope` (0 for FRT_ROPE_NONE or bad input). */
+size_t frt_rope_table_bytes(const frt_rope *rope);
+
+/*
+ * Fill host memory `host_out` (frt_rope_table_bytes(rope) bytes) with the
+ * rotary table: for each axis a in order, for pos < max_pos[a] and pair
+ * i < axis_dims[a]/2, the float pair (cos(pos*theta), sin(pos*theta)) with
+ * theta = base^(-2i/axis_dims[a]); cos/sin are evaluated in double by the C
+ * library and rounded to float. The caller copies it to device memory and
+ * sets rope->table. Host-only; launches nothing.
+ */
+frt_status frt_rope_table_fill(const frt_rope *rope, float *host_out, size_t bytes);
+
+/*
+ * Append n_new tokens to every stream (a write of the persistent state).
+ *   k_new, v_new: bf16 [num_streams][n_new][num_kv_heads][head_dim], device.
+ * For stream b with L = seq_len[b] and i < n_new: slot (L+i) mod capacity
+ * receives K = bf16(fp32(rot_fp64(k_new, L+i))) and V = v_new (bytes
+ * copied); then seq_len[b] = L + n_new. Other slots keep their bytes.
+ * Requires 1 <= n_new <= capacity (n_new = 0 is a no-op returning FRT_OK).
+ */
+frt_status frt_kv_append(const frt_ring *ring, const frt_rope *rope,
+                         const void *k_new, const void *v_new, int32_t n_new,
+                         void *hip_stream);
+
+/*
+ * Workspace bytes frt_stream_attn_step needs: the chunk's rotated, scaled
+ * queries and own keys and its transposed own values (bf16), rounded up.
+ */
+size_t frt_stream_attn_workspace_bytes(const frt_ring *ring, int32_t n_new,
+                                       int32_t num_q_heads);
+
+/*
+ * One streaming step's attention (a read of the persistent state).
+ *   q    : bf16 [num_streams][n_new][num_q_heads][head_dim]
+ *   k_new, v_new: bf16 [num_streams][n_new][num_kv_heads][head_dim]
+ *   out  : bf16 [num_streams][n_new][num_q_heads][head_dim]
+ *   lse  : float [num_streams][num_q_heads][n_new] natural-log sum-exp of the
+ *          scaled scores, or NULL.
+ * Query head h uses KV head h / (num_q_heads / num_kv_heads). Query i of
+ * stream b is token L+i (L = seq_len[b]); its keys are the ring tokens still
+ * held plus the own tokens L..L+n_new-1, filtered by `mask`. softmax_scale
+ * <= 0 selects 1/sqrt(head_dim). The ring is not modified.
+ * Host-checked: num_q_heads % num_kv_heads == 0; n_new <= capacity;
+ * block-causal window*block <= capacity; causal window-1 <= capacity.
+ * Caller contract: no visible key has been evicted (with an unlimited window
+ * the stream must hold all its tokens, seq_len <= capacity).
+ * Numerics: bf16 inputs, fp32 accumulation, bf16 output.
+ */
+frt_status frt_stream_attn_step(const frt_ring *ring, const frt_rope *rope,
+                                const frt_mask *mask, const void *q,
+                                const void *k_new, const void *v_new,
+                                int32_t n_new, int32_t num_q_heads,
+                                float softmax_scale, void *workspace,
+                                size_t workspace_bytes, void *out, float *lse,
+                                void *hip_stream);
+
+/* Largest number of KV splits a decode call uses (ceil(capacity / 256)). */
+int32_t frt_decode_max_splits(const frt_ring *ring);
+
+/* Workspace bytes frt_decode_attn needs: fp32 partial (max, sum, output)
+ * per stream, KV head, split and query head. */
+size_t frt_decode_workspace_bytes(const frt_ring *ring, int32_t num_q_heads);
+
+/*
+ * One-token decode step for every stream: frt_stream_attn_step with
+ * n_new = 1, computed as split-KV (each split of 256 ring slots yields a
+ * partial max/sum/output per query head) followed by a combine pass that
+ * also adds the own token. Same tensor layouts with n_new = 1.
+ * num_q_heads / num_kv_heads must be <= 16.
+ */
+frt_status frt_decode_attn(const frt_ring *ring, const frt_rope *rope,
+                           const frt_mask *mask, const void *q,
+                           const void *k_new, const void *v_new,
+                           int32_t num_q_heads, float softmax_scale,
+                           void *workspace, size_t workspace_bytes, void *out,
+                           float *lse, void *hip_stream);
+
+/* Static description of a status code. */
+const char *frt_status_str(frt_status status);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char *frt_last_error(void);
+
+/*
+ * Built-in kernel timing. When enabled, every kernel the library launches
+ * is bracketed by HIP events on its stream. frt_timing_query waits for the
+ * recorded events of `kernel` (one of "rope_append", "seq_advance",
+ * "chunk_prep", "chunk_attn", "decode_split", "decode_combine") and returns
+ * their count and summed milliseconds; frt_timing_reset drops all records.
+ */
+frt_status frt_timing_enable(int32_t on);
+frt_status frt_timing_query(const char *kernel, int32_t *count, double *total_ms);
+void frt_timing_reset(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FRT_H_ */

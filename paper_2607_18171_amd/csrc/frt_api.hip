@@ -1,0 +1,449 @@
+// C ABI of libfrt: argument validation, launch planning, rotary tables and
+// built-in kernel timing. See include/frt.h for the contract of each call.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "frt.h"
+#include "frt_launch.hpp"
+
+using namespace frt;
+
+namespace {
+
+thread_local std::string g_err;
+
+frt_status fail(frt_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ---------------------------------------------------------------- timing --
+struct TimingRec {
+  const char *name;
+  hipEvent_t start, stop;
+};
+
+std::mutex g_tmu;
+bool g_timing = false;
+std::vector<TimingRec> g_recs;
+std::vector<hipEvent_t> g_pool;
+
+hipEvent_t take_event() {
+  if (!g_pool.empty()) {
+    hipEvent_t e = g_pool.back();
+    g_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <class F>
+frt_status launch(const char *name, hipStream_t s, F &&f) {
+  hipEvent_t a = nullptr, b = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_tmu);
+    if (g_timing) {
+      a = take_event();
+      b = take_event();
+    }
+  }
+  if (a) (void)hipEventRecord(a, s);
+  hipError_t e = f();
+  if (b) (void)hipEventRecord(b, s);
+  if (a && b) {
+    std::lock_guard<std::mutex> lk(g_tmu);
+    g_recs.push_back({name, a, b});
+  }
+  if (e != hipSuccess) return fail(FRT_ERR_HIP, "%s launch failed: %s", name, hipGetErrorString(e));
+  return FRT_OK;
+}
+
+// ------------------------------------------------------------ validation --
+frt_status check_ring(const frt_ring *r) {
+  if (!r) return fail(FRT_ERR_NULL, "ring is NULL");
+  if (!r->k_ring || !r->v_ring || !r->seq_len) return fail(FRT_ERR_NULL, "ring buffer pointer is NULL");
+  if (r->num_streams < 1 || r->num_kv_heads < 1)
+    return fail(FRT_ERR_SHAPE, "num_streams=%d num_kv_heads=%d must be >= 1", r->num_streams,
+                r->num_kv_heads);
+  if (r->head_dim != 64 && r->head_dim != 128)
+    return fail(r->head_dim > 0 ? FRT_ERR_UNSUPPORTED : FRT_ERR_SHAPE,
+                "head_dim=%d (supported: 64, 128)", r->head_dim);
+  if (r->capacity < 8) return fail(FRT_ERR_SHAPE, "capacity=%d must be >= 8", r->capacity);
+  if (r->capacity % 8) return fail(FRT_ERR_ALIGN, "capacity=%d is not a multiple of 8", r->capacity);
+  if ((size_t)r->capacity * r->head_dim * 2 >= (size_t)1 << 31)
+    return fail(FRT_ERR_SHAPE, "capacity*head_dim*2 must be below 2^31");
+  if (!aligned(r->k_ring, 16) || !aligned(r->v_ring, 16) || !aligned(r->seq_len, 8))
+    return fail(FRT_ERR_ALIGN, "ring buffers must be 16-byte aligned (seq_len 8-byte)");
+  return FRT_OK;
+}
+
+frt_status check_rope(const frt_rope *r, int d) {
+  if (!r) return fail(FRT_ERR_NULL, "rope is NULL");
+  if (r->mode == FRT_ROPE_NONE) return FRT_OK;
+  if (r->mode != FRT_ROPE_1D && r->mode != FRT_ROPE_3D)
+    return fail(FRT_ERR_SHAPE, "rope mode %d unknown", r->mode);
+  if (!(r->base > 0.0)) return fail(FRT_ERR_SHAPE, "rope base must be > 0");
+  const int naxes = r->mode == FRT_ROPE_1D ? 1 : 3;
+  int sum = 0;
+  for (int a = 0; a < naxes; ++a) {
+    if (r->axis_dims[a] < 0 || r->axis_dims[a] % 2)
+      return fail(FRT_ERR_SHAPE, "rope axis_dims[%d]=%d must be even and >= 0", a, r->axis_dims[a]);
+    if (r->axis_dims[a] > 0 && r->max_pos[a] < 1)
+      return fail(FRT_ERR_SHAPE, "rope max_pos[%d]=%d must be >= 1", a, r->max_pos[a]);
+    sum += r->axis_dims[a];
+  }
+  if (sum < 2 || sum > d) return fail(FRT_ERR_SHAPE, "rope dims sum %d must be in [2, head_dim]", sum);
+  if (r->mode == FRT_ROPE_3D && (r->frame_hw[0] < 1 || r->frame_hw[1] < 1))
+    return fail(FRT_ERR_SHAPE, "rope frame_hw must be >= 1");
+  if (!r->table) return fail(FRT_ERR_NULL, "rope table is NULL");
+  if (!aligned(r->table, 8)) return fail(FRT_ERR_ALIGN, "rope table must be 8-byte aligned");
+  return FRT_OK;
+}
+
+frt_status check_mask(const frt_mask *m, int C) {
+  if (!m) return fail(FRT_ERR_NULL, "mask is NULL");
+  if (m->window < 0) return fail(FRT_ERR_SHAPE, "mask window must be >= 0");
+  if (m->kind == FRT_MASK_BLOCK_CAUSAL) {
+    if (m->block < 1) return fail(FRT_ERR_SHAPE, "block-causal block must be >= 1");
+    if ((long long)m->window * m->block > C)
+      return fail(FRT_ERR_CAPACITY, "capacity %d < window %d x block %d", C, m->window, m->block);
+  } else if (m->kind == FRT_MASK_CAUSAL) {
+    if (m->window > 0 && m->window - 1 > C)
+      return fail(FRT_ERR_CAPACITY, "capacity %d < causal window %d - 1", C, m->window);
+  } else {
+    return fail(FRT_ERR_SHAPE, "mask kind %d unknown", m->kind);
+  }
+  return FRT_OK;
+}
+
+frt_status check_io(const void *p, const char *what) {
+  if (!p) return fail(FRT_ERR_NULL, "%s is NULL", what);
+  if (!aligned(p, 16)) return fail(FRT_ERR_ALIGN, "%s must be 16-byte aligned", what);
+  return FRT_OK;
+}
+
+RopeDev rope_dev(const frt_rope *r) {
+  RopeDev d;
+  std::memset(&d, 0, sizeof(d));
+  d.mode = r->mode;
+  if (r->mode == FRT_ROPE_NONE) return d;
+  const int naxes = r->mode == FRT_ROPE_1D ? 1 : 3;
+  size_t off = 0;
+  for (int a = 0; a < naxes; ++a) {
+    d.npairs[a] = r->axis_dims[a] / 2;
+    d.maxpos[a] = d.npairs[a] ? r->max_pos[a] : 1;
+    d.tab[a] = reinterpret_cast<const float2 *>(r->table + off);
+    off += (size_t)(d.npairs[a] ? r->max_pos[a] : 0) * d.npairs[a] * 2;
+  }
+  d.frame_h = r->mode == FRT_ROPE_3D ? r->frame_hw[0] : 1;
+  d.frame_w = r->mode == FRT_ROPE_3D ? r->frame_hw[1] : 1;
+  return d;
+}
+
+double q_multiplier(float softmax_scale, int d) {
+  const double scale = softmax_scale > 0.f ? (double)softmax_scale : 1.0 / std::sqrt((double)d);
+  return scale * 1.4426950408889634;  // log2(e): scores are kept in base-2 units
+}
+
+struct StepLayout {
+  size_t q_off, k_off, v_off, bytes;
+  int n_pad;
+};
+
+StepLayout step_layout(const frt_ring *r, int n, int hq) {
+  StepLayout L;
+  const size_t d = (size_t)r->head_dim;
+  L.n_pad = (int)round_up((size_t)n, kChunkBN);
+  L.q_off = 0;
+  L.k_off = round_up((size_t)r->num_streams * n * hq * d * 2, 256);
+  L.v_off = L.k_off + round_up((size_t)r->num_streams * r->num_kv_heads * L.n_pad * d * 2, 256);
+  L.bytes = L.v_off + round_up((size_t)r->num_streams * r->num_kv_heads * L.n_pad * d * 2, 256);
+  return L;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *frt_status_str(frt_status s) {
+  switch (s) {
+    case FRT_OK: return "ok";
+    case FRT_ERR_NULL: return "null pointer";
+    case FRT_ERR_SHAPE: return "invalid shape";
+    case FRT_ERR_UNSUPPORTED: return "unsupported";
+    case FRT_ERR_CAPACITY: return "ring capacity too small";
+    case FRT_ERR_ALIGN: return "misaligned";
+    case FRT_ERR_WORKSPACE: return "workspace too small";
+    case FRT_ERR_HIP: return "HIP error";
+  }
+  return "unknown status";
+}
+
+const char *frt_last_error(void) { return g_err.c_str(); }
+
+size_t frt_rope_table_bytes(const frt_rope *r) {
+  if (!r || r->mode == FRT_ROPE_NONE) return 0;
+  const int naxes = r->mode == FRT_ROPE_1D ? 1 : (r->mode == FRT_ROPE_3D ? 3 : 0);
+  size_t floats = 0;
+  for (int a = 0; a < naxes; ++a) {
+    if (r->axis_dims[a] <= 0 || r->max_pos[a] <= 0) continue;
+    floats += (size_t)r->max_pos[a] * (r->axis_dims[a] / 2) * 2;
+  }
+  return floats * sizeof(float);
+}
+
+frt_status frt_rope_table_fill(const frt_rope *r, float *out, size_t bytes) {
+  if (!r) return fail(FRT_ERR_NULL, "rope is NULL");
+  if (r->mode == FRT_ROPE_NONE) return FRT_OK;
+  if (r->mode != FRT_ROPE_1D && r->mode != FRT_ROPE_3D)
+    return fail(FRT_ERR_SHAPE, "rope mode %d unknown", r->mode);
+  if (!out) return fail(FRT_ERR_NULL, "table output is NULL");
+  const size_t need = frt_rope_table_bytes(r);
+  if (bytes < need) return fail(FRT_ERR_SHAPE, "table buffer %zu < %zu bytes", bytes, need);
+  const int naxes = r->mode == FRT_ROPE_1D ? 1 : 3;
+  size_t off = 0;
+  for (int a = 0; a < naxes; ++a) {
+    const int D = r->axis_dims[a];
+    if (D <= 0 || r->max_pos[a] <= 0) continue;
+    const int np = D / 2;
+    std::vector<double> theta(np);
+    for (int i = 0; i < np; ++i) theta[i] = std::pow(r->base, -(2.0 * i) / D);
+    for (int pos = 0; pos < r->max_pos[a]; ++pos)
+      for (int i = 0; i < np; ++i) {
+        const double ang = (double)pos * theta[i];
+        out[off++] = (float)std::cos(ang);
+        out[off++] = (float)std::sin(ang);
+      }
+  }
+  return FRT_OK;
+}
+
+frt_status frt_kv_append(const frt_ring *ring, const frt_rope *rope, const void *k_new,
+                         const void *v_new, int32_t n_new, void *stream) {
+  frt_status s;
+  if ((s = check_ring(ring)) != FRT_OK) return s;
+  if ((s = check_rope(rope, ring->head_dim)) != FRT_OK) return s;
+  if (n_new < 0) return fail(FRT_ERR_SHAPE, "n_new=%d < 0", n_new);
+  if (n_new > ring->capacity)
+    return fail(FRT_ERR_CAPACITY, "n_new=%d > capacity=%d", n_new, ring->capacity);
+  if (n_new == 0) return FRT_OK;
+  if ((s = check_io(k_new, "k_new")) != FRT_OK) return s;
+  if ((s = check_io(v_new, "v_new")) != FRT_OK) return s;
+  AppendParams p;
+  p.k_new = static_cast<const uint16_t *>(k_new);
+  p.v_new = static_cast<const uint16_t *>(v_new);
+  p.k_ring = static_cast<uint16_t *>(ring->k_ring);
+  p.v_ring = static_cast<uint16_t *>(ring->v_ring);
+  p.seq_len = ring->seq_len;
+  p.B = ring->num_streams;
+  p.Hkv = ring->num_kv_heads;
+  p.D = ring->head_dim;
+  p.C = ring->capacity;
+  p.n = n_new;
+  const RopeDev rd = rope_dev(rope);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if ((s = launch("rope_append", st, [&] { return launch_rope_append(p, rd, st); })) != FRT_OK)
+    return s;
+  return launch("seq_advance", st, [&] { return launch_seq_advance(ring->seq_len, p.B, n_new, st); });
+}
+
+size_t frt_stream_attn_workspace_bytes(const frt_ring *ring, int32_t n_new, int32_t num_q_heads) {
+  if (!ring || n_new <= 0 || num_q_heads <= 0 || ring->head_dim <= 0) return 0;
+  return step_layout(ring, n_new, num_q_heads).bytes;
+}
+
+frt_status frt_stream_attn_step(const frt_ring *ring, const frt_rope *rope, const frt_mask *mask,
+                                const void *q, const void *k_new, const void *v_new, int32_t n_new,
+                                int32_t num_q_heads, float softmax_scale, void *workspace,
+                                size_t workspace_bytes, void *out, float *lse, void *stream) {
+  frt_status s;
+  if ((s = check_ring(ring)) != FRT_OK) return s;
+  if ((s = check_rope(rope, ring->head_dim)) != FRT_OK) return s;
+  if ((s = check_mask(mask, ring->capacity)) != FRT_OK) return s;
+  if (num_q_heads < 1 || num_q_heads % ring->num_kv_heads)
+    return fail(FRT_ERR_SHAPE, "num_q_heads=%d is not a multiple of num_kv_heads=%d", num_q_heads,
+                ring->num_kv_heads);
+  if (n_new < 0) return fail(FRT_ERR_SHAPE, "n_new=%d < 0", n_new);
+  if (n_new > ring->capacity)
+    return fail(FRT_ERR_CAPACITY, "n_new=%d > capacity=%d", n_new, ring->capacity);
+  if (n_new == 0) return FRT_OK;
+  const int G = num_q_heads / ring->num_kv_heads;
+  if ((size_t)n_new * G * ring->head_dim * 2 >= (size_t)1 << 31)
+    return fail(FRT_ERR_SHAPE, "n_new*G*head_dim*2 must be below 2^31");
+  if ((s = check_io(q, "q")) != FRT_OK) return s;
+  if ((s = check_io(k_new, "k_new")) != FRT_OK) return s;
+  if ((s = check_io(v_new, "v_new")) != FRT_OK) return s;
+  if ((s = check_io(out, "out")) != FRT_OK) return s;
+  if (lse && !aligned(lse, 4)) return fail(FRT_ERR_ALIGN, "lse must be 4-byte aligned");
+  const StepLayout lay = step_layout(ring, n_new, num_q_heads);
+  if (!workspace) return fail(FRT_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", lay.bytes);
+  if (workspace_bytes < lay.bytes)
+    return fail(FRT_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, lay.bytes);
+  if (!aligned(workspace, 256)) return fail(FRT_ERR_ALIGN, "workspace must be 256-byte aligned");
+
+  char *ws = static_cast<char *>(workspace);
+  PrepParams pp;
+  pp.q = static_cast<const uint16_t *>(q);
+  pp.k_new = static_cast<const uint16_t *>(k_new);
+  pp.v_new = static_cast<const uint16_t *>(v_new);
+  pp.seq_len = ring->seq_len;
+  pp.qr = reinterpret_cast<uint16_t *>(ws + lay.q_off);
+  pp.kr = reinterpret_cast<uint16_t *>(ws + lay.k_off);
+  pp.vt = reinterpret_cast<uint16_t *>(ws + lay.v_off);
+  pp.B = ring->num_streams;
+  pp.Hq = num_q_heads;
+  pp.Hkv = ring->num_kv_heads;
+  pp.G = G;
+  pp.D = ring->head_dim;
+  pp.n = n_new;
+  pp.n_pad = lay.n_pad;
+  pp.qmul = q_multiplier(softmax_scale, ring->head_dim);
+
+  AttnParams ap;
+  ap.qr = pp.qr;
+  ap.kr = pp.kr;
+  ap.vt = pp.vt;
+  ap.k_ring = static_cast<const uint16_t *>(ring->k_ring);
+  ap.v_ring = static_cast<const uint16_t *>(ring->v_ring);
+  ap.seq_len = ring->seq_len;
+  ap.out = static_cast<uint16_t *>(out);
+  ap.lse = lse;
+  ap.B = pp.B;
+  ap.Hq = num_q_heads;
+  ap.Hkv = pp.Hkv;
+  ap.G = G;
+  ap.n = n_new;
+  ap.n_pad = lay.n_pad;
+  ap.C = ring->capacity;
+  ap.mask_kind = mask->kind;
+  ap.mask_block = mask->block;
+  ap.mask_window = mask->window;
+  const int BM = 32 * kChunkWaves;
+  ap.row_tiles = (n_new * G + BM - 1) / BM;
+
+  const RopeDev rd = rope_dev(rope);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if ((s = launch("chunk_prep", st, [&] { return launch_chunk_prep(pp, rd, st); })) != FRT_OK)
+    return s;
+  return launch("chunk_attn", st, [&] { return launch_chunk_attn(ap, ring->head_dim, st); });
+}
+
+int32_t frt_decode_max_splits(const frt_ring *ring) {
+  if (!ring || ring->capacity <= 0) return 0;
+  return (ring->capacity + kDecodeSplit - 1) / kDecodeSplit;
+}
+
+size_t frt_decode_workspace_bytes(const frt_ring *ring, int32_t num_q_heads) {
+  if (!ring || ring->num_kv_heads <= 0 || num_q_heads <= 0 || ring->head_dim <= 0) return 0;
+  const int G = num_q_heads / ring->num_kv_heads;
+  return (size_t)ring->num_streams * ring->num_kv_heads * frt_decode_max_splits(ring) *
+         decode_split_floats(G, ring->head_dim) * sizeof(float);
+}
+
+frt_status frt_decode_attn(const frt_ring *ring, const frt_rope *rope, const frt_mask *mask,
+                           const void *q, const void *k_new, const void *v_new,
+                           int32_t num_q_heads, float softmax_scale, void *workspace,
+                           size_t workspace_bytes, void *out, float *lse, void *stream) {
+  frt_status s;
+  if ((s = check_ring(ring)) != FRT_OK) return s;
+  if ((s = check_rope(rope, ring->head_dim)) != FRT_OK) return s;
+  if ((s = check_mask(mask, ring->capacity)) != FRT_OK) return s;
+  if (num_q_heads < 1 || num_q_heads % ring->num_kv_heads)
+    return fail(FRT_ERR_SHAPE, "num_q_heads=%d is not a multiple of num_kv_heads=%d", num_q_heads,
+                ring->num_kv_heads);
+  const int G = num_q_heads / ring->num_kv_heads;
+  if (G > 16) return fail(FRT_ERR_UNSUPPORTED, "decode supports up to 16 query heads per KV head");
+  if ((s = check_io(q, "q")) != FRT_OK) return s;
+  if ((s = check_io(k_new, "k_new")) != FRT_OK) return s;
+  if ((s = check_io(v_new, "v_new")) != FRT_OK) return s;
+  if ((s = check_io(out, "out")) != FRT_OK) return s;
+  if (lse && !aligned(lse, 4)) return fail(FRT_ERR_ALIGN, "lse must be 4-byte aligned");
+  const size_t need = frt_decode_workspace_bytes(ring, num_q_heads);
+  if (!workspace) return fail(FRT_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (workspace_bytes < need)
+    return fail(FRT_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, need);
+  if (!aligned(workspace, 16)) return fail(FRT_ERR_ALIGN, "workspace must be 16-byte aligned");
+
+  DecodeParams p;
+  p.q = static_cast<const uint16_t *>(q);
+  p.k_new = static_cast<const uint16_t *>(k_new);
+  p.v_new = static_cast<const uint16_t *>(v_new);
+  p.k_ring = static_cast<const uint16_t *>(ring->k_ring);
+  p.v_ring = static_cast<const uint16_t *>(ring->v_ring);
+  p.seq_len = ring->seq_len;
+  p.ws = static_cast<float *>(workspace);
+  p.out = static_cast<uint16_t *>(out);
+  p.lse = lse;
+  p.B = ring->num_streams;
+  p.Hq = num_q_heads;
+  p.Hkv = ring->num_kv_heads;
+  p.G = G;
+  p.D = ring->head_dim;
+  p.C = ring->capacity;
+  p.nsplit = frt_decode_max_splits(ring);
+  p.mask_kind = mask->kind;
+  p.mask_block = mask->block;
+  p.mask_window = mask->window;
+  p.qmul = q_multiplier(softmax_scale, ring->head_dim);
+  const RopeDev rd = rope_dev(rope);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if ((s = launch("decode_split", st, [&] { return launch_decode_split(p, rd, st); })) != FRT_OK)
+    return s;
+  return launch("decode_combine", st, [&] { return launch_decode_combine(p, rd, st); });
+}
+
+frt_status frt_timing_enable(int32_t on) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_timing = on != 0;
+  return FRT_OK;
+}
+
+frt_status frt_timing_query(const char *kernel, int32_t *count, double *total_ms) {
+  if (!kernel || !count || !total_ms) return fail(FRT_ERR_NULL, "timing query argument is NULL");
+  std::lock_guard<std::mutex> lk(g_tmu);
+  int c = 0;
+  double tot = 0.0;
+  for (const TimingRec &r : g_recs) {
+    if (std::strcmp(r.name, kernel) != 0) continue;
+    if (hipEventSynchronize(r.stop) != hipSuccess)
+      return fail(FRT_ERR_HIP, "hipEventSynchronize failed");
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess)
+      return fail(FRT_ERR_HIP, "hipEventElapsedTime failed");
+    tot += ms;
+    ++c;
+  }
+  *count = c;
+  *total_ms = tot;
+  return FRT_OK;
+}
+
+void frt_timing_reset(void) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  for (const TimingRec &r : g_recs) {
+    hipEventSynchronize(r.stop);
+    g_pool.push_back(r.start);
+    g_pool.push_back(r.stop);
+  }
+  g_recs.clear();
+}
+
+}  // extern "C"

@@ -1,0 +1,140 @@
+// Ring append (RoPE'd K, transposed V, seq_len advance) and the per-step
+// chunk preparation used by the attention kernel.
+//
+// Both kernels are HBM-bound copies with a rotation in double precision: each
+// block owns 64 consecutive tokens of one (stream, KV head); rows are read and
+// written as 16-byte vectors, and V is transposed through LDS so that the
+// slot-contiguous V ring is written with consecutive lanes on consecutive slots.
+#include "frt_launch.hpp"
+
+namespace frt {
+
+namespace {
+
+template <int D>
+__global__ __launch_bounds__(256) void rope_append_kernel(AppendParams p, RopeDev rope) {
+  constexpr int CH = D / 8;           // 16-byte chunks per row
+  constexpr int VS = D + 2;           // LDS row stride (elements), odd dword count
+  __shared__ uint16_t vs[kAppendTokens * VS];
+  const int tb = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const long long L = p.seq_len[b];
+  const int t0 = tb * kAppendTokens;
+  const int ntok = min(kAppendTokens, p.n - t0);
+  const size_t head = (size_t)b * p.Hkv + kvh;
+
+  for (int idx = threadIdx.x; idx < kAppendTokens * CH; idx += 256) {
+    const int r = idx / CH, c = idx % CH;
+    if (r >= ntok) continue;
+    const int i = t0 + r;
+    const size_t src = (((size_t)b * p.n + i) * p.Hkv + kvh) * D + c * 8;
+    const long long pos = L + i;
+    int co[3];
+    rope_coords(rope, pos, co);
+    const u32x4 x = *reinterpret_cast<const u32x4 *>(p.k_new + src);
+    const u32x4 y = rotate8_round(rope, co, c * 4, x, 1.0);
+    const long long slot = pos % p.C;
+    *reinterpret_cast<u32x4 *>(p.k_ring + (head * p.C + slot) * D + c * 8) = y;
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(p.v_new + src);
+    uint32_t *dst = reinterpret_cast<uint32_t *>(vs + r * VS + c * 8);
+    dst[0] = v[0];
+    dst[1] = v[1];
+    dst[2] = v[2];
+    dst[3] = v[3];
+  }
+  __syncthreads();
+  const int r = threadIdx.x & 63;
+  if (r < ntok) {
+    const long long slot = (L + t0 + r) % p.C;
+    uint16_t *vdst = p.v_ring + head * (size_t)D * p.C + slot;
+    for (int dd = threadIdx.x >> 6; dd < D; dd += 4) vdst[(size_t)dd * p.C] = vs[r * VS + dd];
+  }
+}
+
+__global__ void seq_advance_kernel(int64_t *seq_len, int B, int n) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < B) seq_len[b] += n;
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void chunk_prep_kernel(PrepParams p, RopeDev rope) {
+  constexpr int CH = D / 8;
+  constexpr int VS = D + 2;
+  __shared__ uint16_t vs[kAppendTokens * VS];
+  const int tb = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const long long L = p.seq_len[b];
+  const int t0 = tb * kAppendTokens;
+  const size_t head = (size_t)b * p.Hkv + kvh;
+
+  // own keys (stored-key rounding) and values into LDS; zero padding rows
+  for (int idx = threadIdx.x; idx < kAppendTokens * CH; idx += 256) {
+    const int r = idx / CH, c = idx % CH;
+    const int i = t0 + r;
+    u32x4 y = {0u, 0u, 0u, 0u}, v = {0u, 0u, 0u, 0u};
+    if (i < p.n) {
+      const size_t src = (((size_t)b * p.n + i) * p.Hkv + kvh) * D + c * 8;
+      int co[3];
+      rope_coords(rope, L + i, co);
+      y = rotate8_round(rope, co, c * 4, *reinterpret_cast<const u32x4 *>(p.k_new + src), 1.0);
+      v = *reinterpret_cast<const u32x4 *>(p.v_new + src);
+    }
+    if (i < p.n_pad)
+      *reinterpret_cast<u32x4 *>(p.kr + (head * p.n_pad + i) * D + c * 8) = y;
+    uint32_t *dst = reinterpret_cast<uint32_t *>(vs + r * VS + c * 8);
+    dst[0] = v[0];
+    dst[1] = v[1];
+    dst[2] = v[2];
+    dst[3] = v[3];
+  }
+
+  // queries: row i*G + g of this KV head, rotated and scaled
+  const int G = p.G;
+  const int rows_here = max(0, min(kAppendTokens, p.n - t0)) * G;
+  for (int idx = threadIdx.x; idx < rows_here * CH; idx += 256) {
+    const int rr = idx / CH, c = idx % CH;
+    const int i = t0 + rr / G, g = rr % G;
+    const size_t src = (((size_t)b * p.n + i) * p.Hq + kvh * G + g) * D + c * 8;
+    int co[3];
+    rope_coords(rope, L + i, co);
+    const u32x4 y =
+        rotate8_round(rope, co, c * 4, *reinterpret_cast<const u32x4 *>(p.q + src), p.qmul);
+    *reinterpret_cast<u32x4 *>(p.qr + (head * p.n * G + (size_t)i * G + g) * D + c * 8) = y;
+  }
+  __syncthreads();
+
+  // transposed values: token pairs (2 per thread) x D rows
+  if (t0 < p.n_pad) {
+    const int ip = threadIdx.x & 31;
+    uint16_t *vbase = p.vt + head * (size_t)D * p.n_pad + t0 + 2 * ip;
+    for (int dd = threadIdx.x >> 5; dd < D; dd += 8) {
+      const uint32_t lo = vs[(2 * ip) * VS + dd], hi = vs[(2 * ip + 1) * VS + dd];
+      *reinterpret_cast<uint32_t *>(vbase + (size_t)dd * p.n_pad) = lo | (hi << 16);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_rope_append(const AppendParams &p, const RopeDev &r, hipStream_t s) {
+  dim3 grid((p.n + kAppendTokens - 1) / kAppendTokens, p.Hkv, p.B);
+  if (p.D == 128)
+    hipLaunchKernelGGL(rope_append_kernel<128>, grid, dim3(256), 0, s, p, r);
+  else
+    hipLaunchKernelGGL(rope_append_kernel<64>, grid, dim3(256), 0, s, p, r);
+  return hipGetLastError();
+}
+
+hipError_t launch_seq_advance(int64_t *seq_len, int B, int n, hipStream_t s) {
+  hipLaunchKernelGGL(seq_advance_kernel, dim3((B + 255) / 256), dim3(256), 0, s, seq_len, B, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_chunk_prep(const PrepParams &p, const RopeDev &r, hipStream_t s) {
+  dim3 grid((p.n_pad + kAppendTokens - 1) / kAppendTokens, p.Hkv, p.B);
+  if (p.D == 128)
+    hipLaunchKernelGGL(chunk_prep_kernel<128>, grid, dim3(256), 0, s, p, r);
+  else
+    hipLaunchKernelGGL(chunk_prep_kernel<64>, grid, dim3(256), 0, s, p, r);
+  return hipGetLastError();
+}
+
+}  // namespace frt

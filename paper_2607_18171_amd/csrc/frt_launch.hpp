@@ -1,0 +1,72 @@
+// Kernel parameter blocks and launchers (internal to libfrt).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "frt_device.hpp"
+
+namespace frt {
+
+struct AppendParams {
+  const uint16_t *k_new;  // [B][n][Hkv][D]
+  const uint16_t *v_new;  // [B][n][Hkv][D]
+  uint16_t *k_ring;       // [B][Hkv][C][D]
+  uint16_t *v_ring;       // [B][Hkv][D][C]
+  int64_t *seq_len;       // [B]
+  int B, Hkv, D, C, n;
+};
+
+struct PrepParams {
+  const uint16_t *q;      // [B][n][Hq][D]
+  const uint16_t *k_new;  // [B][n][Hkv][D]
+  const uint16_t *v_new;  // [B][n][Hkv][D]
+  const int64_t *seq_len;
+  uint16_t *qr;           // [B][Hkv][n*G][D]    rotated, scaled by qmul
+  uint16_t *kr;           // [B][Hkv][n_pad][D]  rotated (stored-key rounding)
+  uint16_t *vt;           // [B][Hkv][D][n_pad]  transposed
+  int B, Hq, Hkv, G, D, n, n_pad;
+  double qmul;            // softmax scale * log2(e)
+};
+
+struct AttnParams {
+  const uint16_t *qr, *kr, *vt;         // prepared chunk (see PrepParams)
+  const uint16_t *k_ring, *v_ring;
+  const int64_t *seq_len;
+  uint16_t *out;                        // [B][n][Hq][D]
+  float *lse;                           // [B][Hq][n] or null
+  int B, Hq, Hkv, G, n, n_pad, C;
+  int mask_kind, mask_block, mask_window;
+  int row_tiles;
+};
+
+struct DecodeParams {
+  const uint16_t *q;       // [B][1][Hq][D]
+  const uint16_t *k_new;   // [B][1][Hkv][D]
+  const uint16_t *v_new;   // [B][1][Hkv][D]
+  const uint16_t *k_ring, *v_ring;
+  const int64_t *seq_len;
+  float *ws;               // partials, see decode_ws_floats
+  uint16_t *out;           // [B][1][Hq][D]
+  float *lse;              // [B][Hq][1] or null
+  int B, Hq, Hkv, G, D, C, nsplit;
+  int mask_kind, mask_block, mask_window;
+  double qmul;
+};
+
+constexpr int kAppendTokens = 64;   // tokens per append / prep block
+constexpr int kChunkBN = 64;        // keys per attention tile
+constexpr int kChunkWaves = 8;      // waves per attention block (32 query rows each)
+constexpr int kDecodeSplit = 256;   // ring slots per decode split
+
+// Floats of decode workspace per (stream, kv head, split): max[G], sum[G], out[G][D].
+__host__ __device__ inline size_t decode_split_floats(int G, int D) { return (size_t)G * (2 + D); }
+
+hipError_t launch_rope_append(const AppendParams &p, const RopeDev &r, hipStream_t s);
+hipError_t launch_seq_advance(int64_t *seq_len, int B, int n, hipStream_t s);
+hipError_t launch_chunk_prep(const PrepParams &p, const RopeDev &r, hipStream_t s);
+hipError_t launch_chunk_attn(const AttnParams &p, int D, hipStream_t s);
+hipError_t launch_decode_split(const DecodeParams &p, const RopeDev &r, hipStream_t s);
+hipError_t launch_decode_combine(const DecodeParams &p, const RopeDev &r, hipStream_t s);
+
+}  // namespace frt

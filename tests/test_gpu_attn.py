@@ -1,0 +1,152 @@
+"""frt_stream_attn_step on the GPU against the fp64 oracle.
+
+Tolerance (bf16 inputs, fp32 accumulation): max|err| <= 1e-2 * max|V| and
+mean|err| <= 1e-3, per case, over every output element computed.
+"""
+import functools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_18171_amd as frt
+from workloads import (WORKLOADS, RopeSpec, MaskSpec, ROPE_1D, ROPE_3D, ROPE_NONE,
+                       MASK_BLOCK_CAUSAL, MASK_CAUSAL, make_case, shrink)
+from gpu_helpers import (to_dev, from_dev, bf16_dev_to_f64, build_rings, gpu_mask,
+                         visible_vmax, check_close)
+
+pytestmark = pytest.mark.gpu
+
+
+def run_step(case, ring, rope, with_lse=True):
+    wl = case.wl
+    q, k, v = to_dev(case.q), to_dev(case.k_new), to_dev(case.v_new)
+    out = torch.empty_like(q)
+    lse = torch.empty((wl.B, wl.Hq, wl.n), dtype=torch.float32, device="cuda") if with_lse else None
+    ws = torch.empty(frt.stream_attn_workspace_bytes(ring, wl.n, wl.Hq), dtype=torch.uint8,
+                     device="cuda")
+    frt.stream_attn_step(ring, rope, gpu_mask(wl), q, k, v, out, ws, lse=lse)
+    torch.cuda.synchronize()
+    return out, lse
+
+
+SMALL = {
+    "video_small": shrink(WORKLOADS["video_1p3b"], Hq=2, Hkv=2, n=72, C=288,
+                          rope=RopeSpec(ROPE_3D, (44, 42, 42), (4, 6)),
+                          mask=MaskSpec(MASK_BLOCK_CAUSAL, 72, 4), prior_steps=6),
+    "video_partial": shrink(WORKLOADS["video_1p3b"], Hq=3, Hkv=3, n=40, C=96,
+                            rope=RopeSpec(ROPE_3D, (44, 42, 42), (2, 4)),
+                            mask=MaskSpec(MASK_BLOCK_CAUSAL, 40, 2), prior_steps=1),
+    "gqa_swa": shrink(WORKLOADS["prefill_swa"], B=3, Hq=8, Hkv=2, n=100, C=256,
+                      mask=MaskSpec(MASK_CAUSAL, 0, 200), len_lo=0, len_hi=800),
+    "mha_causal": shrink(WORKLOADS["prefill_swa"], B=2, Hq=4, Hkv=4, n=37, C=512,
+                         mask=MaskSpec(MASK_CAUSAL, 0, 0), len_lo=0, len_hi=400),
+    "gqa_d64": shrink(WORKLOADS["prefill_swa"], B=2, Hq=6, Hkv=3, d=64, n=65, C=136,
+                      rope=RopeSpec(ROPE_1D, (64, 0, 0)), mask=MaskSpec(MASK_CAUSAL, 0, 120),
+                      len_lo=0, len_hi=500),
+    "g8_block": shrink(WORKLOADS["prefill_swa"], B=1, Hq=16, Hkv=2, n=48, C=96,
+                       mask=MaskSpec(MASK_BLOCK_CAUSAL, 48, 2), len_lo=96, len_hi=96),
+    "rope_none": shrink(WORKLOADS["prefill_swa"], B=2, Hq=2, Hkv=1, n=33, C=64,
+                        rope=RopeSpec(ROPE_NONE), mask=MaskSpec(MASK_CAUSAL, 0, 50),
+                        len_lo=0, len_hi=300),
+}
+
+
+@pytest.mark.parametrize("name", ["tiny"] + sorted(SMALL))
+@pytest.mark.parametrize("seed", [0, 1])
+def test_small_cases_all_rows(name, seed):
+    wl = WORKLOADS[name] if name in WORKLOADS else SMALL[name]
+    case = make_case(wl, seed)
+    ring, oring, rope = build_rings(case)
+    out, lse = run_step(case, ring, rope)
+    ref, ref_lse = oracle.stream_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask)
+    check_close(bf16_dev_to_f64(out), ref, visible_vmax(oring, case), name)
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() < 2e-2
+    # attention reads the ring, never writes it
+    assert np.array_equal(from_dev(ring.k), oring.k)
+
+
+def test_straddle_chunk_causal():
+    wl = shrink(WORKLOADS["prefill_swa"], B=1, Hq=4, Hkv=2, n=64, C=192,
+                mask=MaskSpec(MASK_CAUSAL, 0, 150))
+    case = make_case(wl, 3, lengths=np.array([160]))
+    ring, oring, rope = build_rings(case)
+    out, _ = run_step(case, ring, rope)
+    ref, _ = oracle.stream_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask)
+    check_close(bf16_dev_to_f64(out), ref, visible_vmax(oring, case), "straddle")
+
+
+def _sample_rows(wl, rng, extra):
+    rows = {0, wl.n - 1, wl.n // 2, 255, 256, 511}
+    rows |= set(int(x) for x in rng.integers(0, wl.n, extra))
+    return np.array(sorted(r for r in rows if 0 <= r < wl.n))
+
+
+@pytest.mark.parametrize("name", ["video_1p3b", "video_14b", "prefill_swa"])
+def test_full_size_sampled_rows(name):
+    wl = WORKLOADS[name]
+    case = make_case(wl, 0)
+    ring, oring, rope = build_rings(case)
+    out, lse = run_step(case, ring, rope)
+    rows = _sample_rows(wl, np.random.default_rng(1), 24)
+    ref, ref_lse = oracle.stream_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask,
+                                      rows=rows)
+    got = bf16_dev_to_f64(out)
+    check_close(got[:, rows], ref[:, rows], visible_vmax(oring, case), name)
+    assert np.abs(lse.cpu().numpy()[:, :, rows] - ref_lse[:, :, rows]).max() < 2e-2
+    assert np.all(np.isfinite(got))
+
+
+def test_v_all_ones_gives_ones():
+    wl = SMALL["gqa_swa"]
+    case = make_case(wl, 4)
+    case.v_new[:] = 0x3F80
+    for k, v in case.prior_fills:
+        v[:] = 0x3F80
+    ring, oring, rope = build_rings(case)
+    out, _ = run_step(case, ring, rope)
+    assert np.abs(bf16_dev_to_f64(out) - 1.0).max() <= 8e-3
+
+
+def test_poisoned_invisible_slots_do_not_change_output():
+    """Never-written and out-of-window slots filled with +-3e4: output bitwise unchanged."""
+    wl = SMALL["gqa_swa"]
+    case = make_case(wl, 5, lengths=np.array([0, 120, 700]))
+    ring, oring, rope = build_rings(case)
+    base, _ = run_step(case, ring, rope)
+    k = ring.k.clone()
+    v = ring.v.clone()
+    # stream 0: nothing written; stream 1: slots >= 120 never written;
+    # stream 2: L=700, window 200: tokens < 700-199 are invisible to every query
+    poison = torch.tensor(29952.0, dtype=torch.bfloat16)
+    ring.k[0] = poison
+    ring.v[0] = -poison
+    ring.k[1, :, 120:] = poison
+    ring.v[1, :, :, 120:] = -poison
+    slots = np.arange(700 - 256, 700 - 199) % 256
+    ring.k[2, :, torch.from_numpy(slots).cuda()] = poison
+    ring.v[2, :, :, torch.from_numpy(slots).cuda()] = -poison
+    out, _ = run_step(case, ring, rope)
+    assert torch.equal(out.view(torch.int16), base.view(torch.int16))
+    ring.k.copy_(k)
+    ring.v.copy_(v)
+
+
+def test_deterministic_and_checkpoint_restore():
+    """Two identical steps give identical bits; a ring copied mid-stream continues identically."""
+    wl = SMALL["video_small"]
+    case = make_case(wl, 6)
+    ring, oring, rope = build_rings(case, extra_tokens=2 * wl.n)
+    a, _ = run_step(case, ring, rope)
+    b, _ = run_step(case, ring, rope)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    saved = frt.Ring(wl.B, wl.Hkv, wl.d, wl.C, k=ring.k.clone(), v=ring.v.clone(),
+                     seq_len=ring.seq_len.clone())
+    for r in (ring, saved):
+        frt.kv_append(r, rope, to_dev(case.k_new), to_dev(case.v_new))
+    x, _ = run_step(case, ring, rope)
+    y, _ = run_step(case, saved, rope)
+    assert torch.equal(x.view(torch.int16), y.view(torch.int16))
+    assert torch.equal(ring.k.view(torch.int16), saved.k.view(torch.int16))
+    assert torch.equal(ring.v.view(torch.int16), saved.v.view(torch.int16))
