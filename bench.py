@@ -104,7 +104,19 @@ def main(argv=None):
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-rows", type=int, default=256,
                     help="query tokens per stream in the oracle's timed sample (0 = skip)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only copy a MIB-sized device buffer 3 times (known HBM traffic for "
+                         "scaling FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args(argv)
+    if args.copy_calibration:
+        import torch
+        a = torch.ones(args.copy_calibration << 18, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_per_launch": a.numel() * 4}))
+        return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the chunk step runs on one MI355X and nothing "

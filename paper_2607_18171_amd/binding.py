@@ -66,6 +66,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     if not os.path.exists(path):
         raise ImportError("libfrt.so not built at %s (run python -m paper_2607_18171_amd.build)"
                           % path)
+    # torch first: libfrt then binds to the HIP runtime torch already loaded,
+    # so both share one runtime, one device context and the same streams.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     P = ctypes.c_void_p
     I32 = ctypes.c_int32

@@ -336,8 +336,7 @@ frt_status frt_stream_attn_step(const frt_ring *ring, const frt_rope *rope, cons
   ap.mask_kind = mask->kind;
   ap.mask_block = mask->block;
   ap.mask_window = mask->window;
-  const int BM = 32 * kChunkWaves;
-  ap.row_tiles = (n_new * G + BM - 1) / BM;
+  ap.row_tiles = (n_new * G + kChunkRows - 1) / kChunkRows;
 
   const RopeDev rd = rope_dev(rope);
   hipStream_t st = static_cast<hipStream_t>(stream);

@@ -1,15 +1,23 @@
 // Chunk-streamed attention: one block per (stream, KV head, tile of 32*NW
 // query rows), rows ordered (token, query head of the group). Each wave owns
 // 32 query rows and computes S^T = K Q^T with bf16 32x32x16 MFMAs, so every
-// lane holds the scores of one query row: the online-softmax max/sum stays in
-// the lane except for one exchange with the lane 32 away. O^T = V^T P^T reuses
-// the score registers directly as the B operand.
+// lane holds the scores of one query row: the online-softmax max and sum stay
+// in the lane except for one exchange with the lane 32 away
+// (v_permlane32_swap). O^T = V^T P^T reuses the score registers directly as
+// the B operand.
 //
 // Keys come from up to three runs: at most two physical runs of ring slots
-// (the visible token range wraps at most once) and the chunk's own keys.
-// Tiles of 64 keys are staged in LDS (double buffered: the next tile's global
-// loads are issued before the current tile's MFMAs). Tiles wholly visible to
-// every row of the block skip masking.
+// (the visible token range wraps at most once) and the chunk's own keys,
+// processed in tiles of 64 keys staged in LDS. Tiles wholly visible to every
+// row of the block skip masking.
+//
+// Software pipeline. Iteration t issues the QK MFMAs of tile t+1 next to the
+// softmax VALU work of tile t, then the PV MFMAs of tile t next to the row
+// max of tile t+1, so each wave keeps the matrix pipe fed while it does its
+// vector work. K therefore runs one tile ahead of V in LDS: iteration t reads
+// K(t+1) and V(t) while the global loads of K(t+2) and V(t+1) are in flight
+// (both double buffered). Masking of edge tiles and the rare rescale of the
+// running max happen between iterations, outside that instruction stream.
 //
 // Operand layout. For the 32x32x16 MFMA the accumulator register r of lane l
 // holds row 8*(r/4) + 4*(l/32) + r%4 and column l%32. The K tile row loaded
@@ -17,14 +25,41 @@
 // makes register r of key block kb hold key 32*kb + 16*(r/8) + 8*(l/32) + r%8:
 // the 8 scores a lane feeds to one PV MFMA are 8 consecutive keys, so the V^T
 // operand is one contiguous 16-byte LDS read.
+//
+// Online softmax in base-2 units (queries arrive pre-scaled by
+// scale*log2(e)) with a lazily raised reference max m per row: m moves only
+// when a tile's max exceeds it by more than kTau, or at the row's first
+// visible key, so weights stay below 2^kTau and the O rescale is rare.
 #include "frt_launch.hpp"
 
 namespace frt {
 
 namespace {
 
+// value (not reference) selection: keeps the selected variables in registers
+template <class T>
+__device__ __forceinline__ T pick(bool c, T a, T b) {
+  return c ? a : b;
+}
+
 __device__ __forceinline__ int perm23(int x) {
   return (x & ~0xC) | ((x & 4) << 1) | ((x & 8) >> 1);
+}
+
+// max of x over lanes l and l^32
+__device__ __forceinline__ float max_pair32(float x) {
+  const u32x2 r = __builtin_bit_cast(
+      u32x2, __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                              false));
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// sum of x over lanes l and l^32
+__device__ __forceinline__ float sum_pair32(float x) {
+  const u32x2 r = __builtin_bit_cast(
+      u32x2, __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                              false));
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 template <int D, int NW>
@@ -34,37 +69,47 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
   constexpr int NT = NW * 64;
   constexpr int KST = D + 8;   // K tile row stride (elements)
   constexpr int VST = BN + 8;  // V^T tile row stride (elements)
-  constexpr int KCH = BN * D / 8;
-  constexpr int VCH = D * BN / 8;
-  constexpr int KPT = KCH / NT;
-  constexpr int VPT = VCH / NT;
+  constexpr int KPT = BN * D / 8 / NT;
+  constexpr int VPT = D * BN / 8 / NT;
+  constexpr float kTau = 8.f;
+  constexpr float kNegInf = -__builtin_inff();
   static_assert(KPT >= 1 && VPT >= 1, "tile too small for the block");
   __shared__ __attribute__((aligned(16))) uint16_t ks[2][BN * KST];
   __shared__ __attribute__((aligned(16))) uint16_t vs[2][D * VST];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, h = lane >> 5;
-  const int rt = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+
+  // Blocks are dealt to the 8 XCDs round robin; give each XCD a contiguous
+  // range of logical tiles (row tiles of one head are adjacent) so the
+  // blocks sharing a head's K/V tiles share one L2.
+  const int nlog = p.row_tiles * p.Hkv * p.B;
+  const int jlog = (int)(blockIdx.x % 8) * (int)(gridDim.x / 8) + (int)(blockIdx.x / 8);
+  if (jlog >= nlog) return;
+  const int rt = jlog % p.row_tiles;
+  const int kvh = (jlog / p.row_tiles) % p.Hkv;
+  const int b = jlog / (p.row_tiles * p.Hkv);
+
   const long long L = p.seq_len[b];
   const int G = p.G, n = p.n, C = p.C;
   const int rows = n * G;
   const int row0 = rt * BM;
   const int myrow = row0 + wave * 32 + l32;
-  const int myi = min(myrow, rows - 1) / G;
   const int i_lo = row0 / G;
   const int i_hi = (min(row0 + BM, rows) - 1) / G;
 
-  // visibility, relative to L
+  // visibility, relative to L: this lane's row [vlo, vhi]; the block's union
+  // [ulo, uhi] and intersection [ilo, ihi]
   long long lo, hi;
-  visible_range(p.mask_kind, p.mask_block, p.mask_window, L + myi, lo, hi);
+  visible_range(p.mask_kind, p.mask_block, p.mask_window, L + min(myrow, rows - 1) / G, lo, hi);
   const int vlo = clamp_i32(lo - L), vhi = clamp_i32(hi - L);
   visible_range(p.mask_kind, p.mask_block, p.mask_window, L + i_lo, lo, hi);
   const int ulo = clamp_i32(lo - L), ihi = clamp_i32(hi - L);
   visible_range(p.mask_kind, p.mask_block, p.mask_window, L + i_hi, lo, hi);
   const int ilo = clamp_i32(lo - L), uhi = clamp_i32(hi - L);
 
-  const int lc = (int)(L < C ? L : (long long)C);     // ring tokens held
-  const int hh = (int)(L % C);                         // slot of token L
+  const int lc = (int)(L < C ? L : (long long)C);  // ring tokens held
+  const int hh = (int)(L % C);                      // slot of token L
   // relative token of ring slot s: s-hh (s < hh) or s-hh-C (s >= hh)
 
   // runs of keys: ring run 0 [ra0, re0), ring run 1 [ra1, re1), own run [oa, oe)
@@ -96,6 +141,7 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
   const int c0 = re0 > ra0 ? (re0 - rf0 + BN - 1) / BN : 0;
   const int c1 = re1 > ra1 ? (re1 - rf1 + BN - 1) / BN : 0;
   const int c2 = oe > oa ? (oe - of + BN - 1) / BN : 0;
+  const int T = c0 + c1 + c2;
 
   const size_t head = (size_t)b * p.Hkv + kvh;
   const __amdgpu_buffer_rsrc_t rk_ring =
@@ -125,64 +171,63 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
-  float m = -__builtin_inff();
-  float lsum = 0.f;
+  float m = 0.f, lsum = 0.f;
+  bool mset = false;
+
+  // ---- tile bookkeeping (block-uniform, scalar) ----
+  // tile t -> run (0, 1: ring; 2: own) and first key (slot or own index)
+  auto tile_run = [&](int t) __attribute__((always_inline)) {
+    return t < c0 ? 0 : (t < c0 + c1 ? 1 : 2);
+  };
+  auto tile_base = [&](int t) __attribute__((always_inline)) {
+    return t < c0 ? rf0 + t * BN : (t < c0 + c1 ? rf1 + (t - c0) * BN : of + (t - c0 - c1) * BN);
+  };
+  auto tile_fast = [&](int t) __attribute__((always_inline)) {
+    const int run = tile_run(t), base = tile_base(t), end = base + BN;
+    if (run == 2) return base >= oa && end <= oe && base >= ilo && end - 1 <= ihi;
+    const int ra = pick(run == 0, ra0, ra1), re = pick(run == 0, re0, re1);
+    int kmin, kmax;
+    if (base < hh && hh < end) {
+      kmin = -C;
+      kmax = -1;
+    } else {
+      kmin = base < hh ? base - hh : base - hh - C;
+      kmax = (end - 1) < hh ? end - 1 - hh : end - 1 - hh - C;
+    }
+    return base >= ra && end <= re && end <= C && kmin >= max(ilo, -lc) && kmax <= ihi;
+  };
 
   u32x4 kreg[KPT], vreg[VPT];
-
-  // tile t -> run (0, 1: ring; 2: own) and first key (slot or own index)
-  auto tile_of = [&](int t, int &run, int &base) {
-    if (t < c0) {
-      run = 0;
-      base = rf0 + t * BN;
-    } else if (t < c0 + c1) {
-      run = 1;
-      base = rf1 + (t - c0) * BN;
-    } else {
-      run = 2;
-      base = of + (t - c0 - c1) * BN;
+  auto load_k = [&](int t) __attribute__((always_inline)) {
+    const int run = tile_run(t), base = tile_base(t);
+    const __amdgpu_buffer_rsrc_t rk = pick(run == 2, rk_own, rk_ring);
+#pragma unroll
+    for (int u = 0; u < KPT; ++u) {
+      const int idx = tid + NT * u;
+      const int kr = idx / (D / 8), kc = idx % (D / 8);
+      kreg[u] = buf_load16(rk, (uint32_t)(((size_t)(base + kr) * D + kc * 8) * 2));
     }
   };
-
-  auto load_tile = [&](int t) {
-    int run, base;
-    tile_of(t, run, base);
-    if (run != 2) {
+  auto load_v = [&](int t) __attribute__((always_inline)) {
+    const int run = tile_run(t), base = tile_base(t);
+    const __amdgpu_buffer_rsrc_t rv = pick(run == 2, rv_own, rv_ring);
+    const int vstride = pick(run == 2, p.n_pad, C);
 #pragma unroll
-      for (int u = 0; u < KPT; ++u) {
-        const int idx = tid + NT * u;
-        const int kr = idx / (D / 8), kc = idx % (D / 8);
-        kreg[u] = buf_load16(rk_ring, (uint32_t)(((size_t)(base + kr) * D + kc * 8) * 2));
-      }
-#pragma unroll
-      for (int u = 0; u < VPT; ++u) {
-        const int idx = tid + NT * u;
-        const int dd = idx / (BN / 8), vc = idx % (BN / 8);
-        vreg[u] = buf_load16(rv_ring, (uint32_t)(((size_t)dd * C + base + vc * 8) * 2));
-      }
-    } else {
-#pragma unroll
-      for (int u = 0; u < KPT; ++u) {
-        const int idx = tid + NT * u;
-        const int kr = idx / (D / 8), kc = idx % (D / 8);
-        kreg[u] = buf_load16(rk_own, (uint32_t)(((size_t)(base + kr) * D + kc * 8) * 2));
-      }
-#pragma unroll
-      for (int u = 0; u < VPT; ++u) {
-        const int idx = tid + NT * u;
-        const int dd = idx / (BN / 8), vc = idx % (BN / 8);
-        vreg[u] = buf_load16(rv_own, (uint32_t)(((size_t)dd * p.n_pad + base + vc * 8) * 2));
-      }
+    for (int u = 0; u < VPT; ++u) {
+      const int idx = tid + NT * u;
+      const int dd = idx / (BN / 8), vc = idx % (BN / 8);
+      vreg[u] = buf_load16(rv, (uint32_t)(((size_t)dd * vstride + base + vc * 8) * 2));
     }
   };
-
-  auto store_tile = [&](int buf) {
+  auto store_k = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < KPT; ++u) {
       const int idx = tid + NT * u;
       const int kr = idx / (D / 8), kc = idx % (D / 8);
       *reinterpret_cast<u32x4 *>(&ks[buf][kr * KST + kc * 8]) = kreg[u];
     }
+  };
+  auto store_v = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < VPT; ++u) {
       const int idx = tid + NT * u;
@@ -191,119 +236,145 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
     }
   };
 
-  const int T = c0 + c1 + c2;
-  if (T > 0) {
-    load_tile(0);
-    store_tile(0);
-  }
-  __syncthreads();
-
+  // ---- per-wave compute pieces ----
   const int prow = perm23(l32);
-  for (int t = 0; t < T; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < T) load_tile(t + 1);
-
-    int run, base;
-    tile_of(t, run, base);
-    const int ra = run == 0 ? ra0 : (run == 1 ? ra1 : oa);
-    const int re = run == 0 ? re0 : (run == 1 ? re1 : oe);
-    const bool own = run == 2;
-    bool fast;
-    if (own) {
-      fast = base >= ra && base + BN <= re && base >= ilo && base + BN - 1 <= ihi;
-    } else {
-      const int end = base + BN;
-      int kmin, kmax;
-      if (base < hh && hh < end) {
-        kmin = -C;
-        kmax = -1;
-      } else {
-        kmin = base < hh ? base - hh : base - hh - C;
-        kmax = (end - 1) < hh ? end - 1 - hh : end - 1 - hh - C;
-      }
-      fast = base >= ra && end <= re && end <= C && kmin >= max(ilo, -lc) && kmax <= ihi;
-    }
-
-    // S^T = K Q^T for two blocks of 32 keys
-    f32x16 sacc[2];
+  // S^T for the 64 keys of K buffer kbuf
+  auto qk = [&](int kbuf, f32x16 (&s)[2]) __attribute__((always_inline)) {
+    const f32x16 zero = {};
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
+      const uint16_t *krow = &ks[kbuf][(32 * kb + prow) * KST + 8 * h];
+      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+          *reinterpret_cast<const bf16x8 *>(krow), qf[0], zero, 0, 0, 0);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
-      const uint16_t *krow = &ks[buf][(32 * kb + prow) * KST + 8 * h];
-#pragma unroll
-      for (int k = 0; k < D / 16; ++k) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(krow + 16 * k);
-        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[k], sacc[kb], 0, 0, 0);
-      }
+      for (int k = 1; k < D / 16; ++k)
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            *reinterpret_cast<const bf16x8 *>(krow + 16 * k), qf[k], s[kb], 0, 0, 0);
     }
-
-    if (!fast) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int off = 32 * kb + 16 * (r >> 3) + 8 * h + (r & 7);
-          const int s = base + off;
-          bool ok;
-          if (own) {
-            ok = s >= ra && s < re && s >= vlo && s <= vhi;
-          } else {
-            const int krel = s < hh ? s - hh : s - hh - C;
-            ok = s >= ra && s < re && s < C && krel >= -lc && krel >= vlo && krel <= vhi;
-          }
-          if (!ok) sacc[kb][r] = -__builtin_inff();
-        }
-      }
-    }
-
-    float mt = sacc[0][0];
+  };
+  auto row_max = [&](const f32x16 (&s)[2]) __attribute__((always_inline)) {
+    float mt = fmaxf(s[0][0], s[0][1]);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mt = fmaxf(mt, sacc[kb][r]);
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float mnew = fmaxf(m, mt);
-    const float msafe = mnew == -__builtin_inff() ? 0.f : mnew;
-    const float alpha = __builtin_amdgcn_exp2f(m - msafe);
-    m = mnew;
-
-    float ts = 0.f;
-    bf16x8 pf[2][2];
+      for (int r = 0; r < 16; r += 2) mt = fmaxf(mt, fmaxf(s[kb][r], s[kb][r + 1]));
+    return max_pair32(mt);
+  };
+  auto mask_tile = [&](int t, f32x16 (&s)[2]) __attribute__((always_inline)) {
+    const int run = tile_run(t), base = tile_base(t);
+    const int ra = pick(run == 0, ra0, pick(run == 1, ra1, oa));
+    const int re = pick(run == 0, re0, pick(run == 1, re1, oe));
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float e = __builtin_amdgcn_exp2f(sacc[kb][r] - msafe);
-        ts += e;
-        pf[kb][r >> 3][r & 7] = (__bf16)e;
+        const int sl = base + 32 * kb + 16 * (r >> 3) + 8 * h + (r & 7);
+        const int krel = run == 2 ? sl : (sl < hh ? sl - hh : sl - hh - C);
+        const bool ok = sl >= ra && sl < re && (run == 2 || (sl < C && krel >= -lc)) &&
+                        krel >= vlo && krel <= vhi;
+        s[kb][r] = ok ? s[kb][r] : kNegInf;
       }
-    lsum = lsum * alpha + ts;
-    if (__ballot(alpha != 1.f)) {
+  };
+  // raise the reference max when the tile's max exceeds it (rare, uniform branch)
+  auto rescale = [&](float mt) __attribute__((always_inline)) {
+    const float rel = mt - m;
+    const bool need = rel > kTau || (!mset && mt != kNegInf);
+    if (__ballot(need)) {
+      const float delta = need ? rel : 0.f;
+      const float alpha = __builtin_amdgcn_exp2f(-delta);
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+      lsum *= alpha;
+      m += delta;
+      mset = mset || need;
     }
-
-    // O^T += V^T P^T
+  };
+  const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
+  auto softmax = [&](const f32x16 (&s)[2], bf16x8 (&pf)[2][2]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-      const uint16_t *vrow = &vs[buf][(32 * db + l32) * VST + 8 * h];
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int r = 0; r < 16; ++r)
+        pf[kb][r >> 3][r & 7] = (__bf16)__builtin_amdgcn_exp2f(s[kb][r] - m);
+    // row sum of the rounded weights the PV product uses
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(vrow + 32 * kb + 16 * j);
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][j], o[db], 0, 0, 0);
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const bf16x2 pr = {pf[kb][jj][2 * w], pf[kb][jj][2 * w + 1]};
+          lsum = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, lsum, false);
         }
-    }
+  };
+  auto pv = [&](int vbuf, const bf16x8 (&pf)[2][2]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        const uint16_t *vrow = &vs[vbuf][(32 * db + l32) * VST + 8 * h + 32 * kb];
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8 *>(vrow),
+                                                        pf[kb][0], o[db], 0, 0, 0);
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            *reinterpret_cast<const bf16x8 *>(vrow + 16), pf[kb][1], o[db], 0, 0, 0);
+      }
+  };
 
-    if (t + 1 < T) store_tile(buf ^ 1);
+  // One pipelined iteration for a tile t that has a successor: QK(t+1) with
+  // softmax(t), PV(t) with max(t+1); stage K(t+2) and V(t+1) into LDS.
+  auto step = [&](int t, f32x16 (&scur)[2], f32x16 (&snext)[2]) __attribute__((always_inline)) {
+    load_k(min(t + 2, T - 1));
+    load_v(t + 1);
+    bf16x8 pf[2][2];
+    qk((t + 1) & 1, snext);
+    softmax(scur, pf);
+    pv(t & 1, pf);
+    float mt = row_max(snext);
+    store_k(t & 1);
+    store_v((t + 1) & 1);
+    if (!tile_fast(t + 1)) {
+      mask_tile(t + 1, snext);
+      mt = row_max(snext);
+    }
+    rescale(mt);
     __syncthreads();
+  };
+
+  f32x16 sa[2], sb[2];
+  if (T > 0) {
+    load_k(0);
+    load_v(0);
+    store_k(0);
+    store_v(0);
+    if (T > 1) {
+      load_k(1);
+      store_k(1);
+    }
+    __syncthreads();
+    qk(0, sa);
+    if (!tile_fast(0)) mask_tile(0, sa);
+    rescale(row_max(sa));
+    __syncthreads();  // K buffer 0 is refilled by the first step
+
+    int t = 0;
+    for (; t + 2 < T; t += 2) {
+      step(t, sa, sb);
+      step(t + 1, sb, sa);
+    }
+    bf16x8 pf[2][2];
+    if (t + 1 < T) {  // two tiles left
+      step(t, sa, sb);
+      softmax(sb, pf);
+      pv((t + 1) & 1, pf);
+    } else {  // one tile left
+      softmax(sa, pf);
+      pv(t & 1, pf);
+    }
   }
 
-  const float ltot = lsum + __shfl_xor(lsum, 32);
+  const float ltot = sum_pair32(lsum);
   if (myrow < rows) {
     const float inv = 1.f / ltot;
     const int i = myrow / G, g = myrow % G;
@@ -329,13 +400,13 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
 }  // namespace
 
 hipError_t launch_chunk_attn(const AttnParams &p, int D, hipStream_t s) {
-  dim3 grid(p.row_tiles, p.Hkv, p.B);
+  const int nlog = p.row_tiles * p.Hkv * p.B;
+  dim3 grid((nlog + 7) / 8 * 8);
+  dim3 block(kChunkWaves * 64);
   if (D == 128)
-    hipLaunchKernelGGL((chunk_attn_kernel<128, kChunkWaves>), grid, dim3(kChunkWaves * 64), 0, s,
-                       p);
+    hipLaunchKernelGGL((chunk_attn_kernel<128, kChunkWaves>), grid, block, 0, s, p);
   else
-    hipLaunchKernelGGL((chunk_attn_kernel<64, kChunkWaves>), grid, dim3(kChunkWaves * 64), 0, s,
-                       p);
+    hipLaunchKernelGGL((chunk_attn_kernel<64, kChunkWaves>), grid, block, 0, s, p);
   return hipGetLastError();
 }
 

@@ -56,7 +56,11 @@ struct DecodeParams {
 
 constexpr int kAppendTokens = 64;   // tokens per append / prep block
 constexpr int kChunkBN = 64;        // keys per attention tile
-constexpr int kChunkWaves = 8;      // waves per attention block (32 query rows each)
+#ifndef FRT_ATTN_WAVES
+#define FRT_ATTN_WAVES 8
+#endif
+constexpr int kChunkWaves = FRT_ATTN_WAVES;  // waves per attention block
+constexpr int kChunkRows = 32 * kChunkWaves;  // query rows per block (32 per wave)
 constexpr int kDecodeSplit = 256;   // ring slots per decode split
 
 // Floats of decode workspace per (stream, kv head, split): max[G], sum[G], out[G][D].
