@@ -113,6 +113,8 @@ frt_status check_rope(const frt_rope *r, int d) {
   if (sum < 2 || sum > d) return fail(FRT_ERR_SHAPE, "rope dims sum %d must be in [2, head_dim]", sum);
   if (r->mode == FRT_ROPE_3D && (r->frame_hw[0] < 1 || r->frame_hw[1] < 1))
     return fail(FRT_ERR_SHAPE, "rope frame_hw must be >= 1");
+  if (frt_rope_table_bytes(r) >= (size_t)1 << 31)
+    return fail(FRT_ERR_SHAPE, "rope table must be below 2^31 bytes");
   if (!r->table) return fail(FRT_ERR_NULL, "rope table is NULL");
   if (!aligned(r->table, 8)) return fail(FRT_ERR_ALIGN, "rope table must be 8-byte aligned");
   return FRT_OK;
@@ -144,17 +146,22 @@ RopeDev rope_dev(const frt_rope *r) {
   RopeDev d;
   std::memset(&d, 0, sizeof(d));
   d.mode = r->mode;
+  d.frame_h = d.frame_w = 1;
   if (r->mode == FRT_ROPE_NONE) return d;
   const int naxes = r->mode == FRT_ROPE_1D ? 1 : 3;
-  size_t off = 0;
+  size_t off = 0;  // in (cos, sin) entries
   for (int a = 0; a < naxes; ++a) {
     d.npairs[a] = r->axis_dims[a] / 2;
     d.maxpos[a] = d.npairs[a] ? r->max_pos[a] : 1;
-    d.tab[a] = reinterpret_cast<const float2 *>(r->table + off);
-    off += (size_t)(d.npairs[a] ? r->max_pos[a] : 0) * d.npairs[a] * 2;
+    d.tab_off[a] = (int)off;
+    off += (size_t)(d.npairs[a] ? r->max_pos[a] : 0) * d.npairs[a];
   }
-  d.frame_h = r->mode == FRT_ROPE_3D ? r->frame_hw[0] : 1;
-  d.frame_w = r->mode == FRT_ROPE_3D ? r->frame_hw[1] : 1;
+  if (r->mode == FRT_ROPE_3D) {
+    d.frame_h = r->frame_hw[0];
+    d.frame_w = r->frame_hw[1];
+  }
+  d.tab_bytes = (uint32_t)frt_rope_table_bytes(r);
+  d.table = reinterpret_cast<const float2 *>(r->table);
   return d;
 }
 
@@ -438,7 +445,7 @@ frt_status frt_timing_query(const char *kernel, int32_t *count, double *total_ms
 void frt_timing_reset(void) {
   std::lock_guard<std::mutex> lk(g_tmu);
   for (const TimingRec &r : g_recs) {
-    hipEventSynchronize(r.stop);
+    (void)hipEventSynchronize(r.stop);
     g_pool.push_back(r.start);
     g_pool.push_back(r.stop);
   }

@@ -16,6 +16,7 @@ __global__ __launch_bounds__(256) void rope_append_kernel(AppendParams p, RopeDe
   constexpr int CH = D / 8;           // 16-byte chunks per row
   constexpr int VS = D + 2;           // LDS row stride (elements), odd dword count
   __shared__ uint16_t vs[kAppendTokens * VS];
+  const RopeReg rg = rope_reg(rope);
   const int tb = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const long long L = p.seq_len[b];
   const int t0 = tb * kAppendTokens;
@@ -29,9 +30,9 @@ __global__ __launch_bounds__(256) void rope_append_kernel(AppendParams p, RopeDe
     const size_t src = (((size_t)b * p.n + i) * p.Hkv + kvh) * D + c * 8;
     const long long pos = L + i;
     int co[3];
-    rope_coords(rope, pos, co);
+    rope_coords(rg, pos, co);
     const u32x4 x = *reinterpret_cast<const u32x4 *>(p.k_new + src);
-    const u32x4 y = rotate8_round(rope, co, c * 4, x, 1.0);
+    const u32x4 y = rotate8_round(rg, co, c * 4, x, 1.0);
     const long long slot = pos % p.C;
     *reinterpret_cast<u32x4 *>(p.k_ring + (head * p.C + slot) * D + c * 8) = y;
     const u32x4 v = *reinterpret_cast<const u32x4 *>(p.v_new + src);
@@ -60,6 +61,7 @@ __global__ __launch_bounds__(256) void chunk_prep_kernel(PrepParams p, RopeDev r
   constexpr int CH = D / 8;
   constexpr int VS = D + 2;
   __shared__ uint16_t vs[kAppendTokens * VS];
+  const RopeReg rg = rope_reg(rope);
   const int tb = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const long long L = p.seq_len[b];
   const int t0 = tb * kAppendTokens;
@@ -73,8 +75,8 @@ __global__ __launch_bounds__(256) void chunk_prep_kernel(PrepParams p, RopeDev r
     if (i < p.n) {
       const size_t src = (((size_t)b * p.n + i) * p.Hkv + kvh) * D + c * 8;
       int co[3];
-      rope_coords(rope, L + i, co);
-      y = rotate8_round(rope, co, c * 4, *reinterpret_cast<const u32x4 *>(p.k_new + src), 1.0);
+      rope_coords(rg, L + i, co);
+      y = rotate8_round(rg, co, c * 4, *reinterpret_cast<const u32x4 *>(p.k_new + src), 1.0);
       v = *reinterpret_cast<const u32x4 *>(p.v_new + src);
     }
     if (i < p.n_pad)
@@ -94,9 +96,9 @@ __global__ __launch_bounds__(256) void chunk_prep_kernel(PrepParams p, RopeDev r
     const int i = t0 + rr / G, g = rr % G;
     const size_t src = (((size_t)b * p.n + i) * p.Hq + kvh * G + g) * D + c * 8;
     int co[3];
-    rope_coords(rope, L + i, co);
+    rope_coords(rg, L + i, co);
     const u32x4 y =
-        rotate8_round(rope, co, c * 4, *reinterpret_cast<const u32x4 *>(p.q + src), p.qmul);
+        rotate8_round(rg, co, c * 4, *reinterpret_cast<const u32x4 *>(p.q + src), p.qmul);
     *reinterpret_cast<u32x4 *>(p.qr + (head * p.n * G + (size_t)i * G + g) * D + c * 8) = y;
   }
   __syncthreads();

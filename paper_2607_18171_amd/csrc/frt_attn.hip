@@ -36,11 +36,6 @@ namespace frt {
 
 namespace {
 
-// value (not reference) selection: keeps the selected variables in registers
-template <class T>
-__device__ __forceinline__ T pick(bool c, T a, T b) {
-  return c ? a : b;
-}
 
 __device__ __forceinline__ int perm23(int x) {
   return (x & ~0xC) | ((x & 4) << 1) | ((x & 8) >> 1);
