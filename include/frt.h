@@ -5,9 +5,10 @@
  * What a streaming step is. The FlashRT paper models a real-time pipeline as
  * a task graph processed batch by batch; a node of batch j may depend on the
  * persistent state its own instance left behind in batch j-1 (Problem
- * Formulation: cross-batch lambda=1 edges, the example being a KV cache that
- * batch j inherits from batch j-1; Chain-of-Program, IR design: node-level
- * persistent-state read/write annotations; appendix "Pipeline graph"). In the
+ * Formulation: cross-batch lambda=1 edges, whose example is an attention
+ * key/value cache carried from one batch to the next; Chain-of-Program, IR
+ * design: node-level persistent-state read/write annotations; appendix
+ * "Formal Analysis of Pipeline Graphs"). In the
  * autoregressive video DiTs and multimodal LLMs the paper deploys, that state
  * is the attention KV cache, and each step's new query chunk attends to the
  * cached keys plus its own. This library implements that step:
@@ -101,7 +102,8 @@ typedef struct {
  *                       (p div HW, (p mod HW) div W, p mod W);
  *                       max_pos = {frames, H, W} held in the table.
  *   base: theta base (10000 in the paper's models).
- *   table: device copy of the buffer written by frt_rope_table_fill.
+ *   table: device copy of the buffer written by frt_rope_table_fill; its size
+ *          frt_rope_table_bytes(rope) must be below 2^31 (FRT_ERR_SHAPE).
  * Contract: every token position rotated by a call lies inside max_pos
  * (positions beyond it are clamped to the last table row, which is wrong but
  * never reads out of bounds).

@@ -10,9 +10,9 @@ What is computed, and where it comes from
 -----------------------------------------
 The paper (FlashRT) defines the *state semantics* of a streaming step: batch j
 of a node reads persistent state written by batch j-1 of the same node and
-writes it for batch j+1 (Problem Formulation: cross-batch lambda=1 edges, "a
-KV cache that batch j inherits from batch j-1"; Chain-of-Program, IR design:
-node-level persistent-state read/write annotations; App. "Pipeline graph";
+writes it for batch j+1 (Problem Formulation: cross-batch lambda=1 edges, with
+a key/value cache carried between batches as the example; Chain-of-Program, IR design:
+node-level persistent-state read/write annotations; App. "Formal Analysis of Pipeline Graphs";
 App. "Application 2": independent per-denoising-step KV caches). It gives no
 arithmetic for the attention itself. The arithmetic here is therefore the
 plain textbook definition:

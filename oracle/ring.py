@@ -6,9 +6,9 @@ worked slot examples in tests/golden/ring_slots.txt, untouched-slot and
 byte-copy invariants).
 
 The persistent state of one stream is what the paper calls state inherited
-across batches (Problem Formulation: lambda=1 edges, "a KV cache that batch j
-inherits from batch j-1"; Chain-of-Program, IR design: a node's persistent
-state reads and writes). Here that state is, per stream b and KV head h, C
+across batches (Problem Formulation: lambda=1 edges, whose example is an
+attention key/value cache carried from one batch to the next; Chain-of-Program,
+IR design: a node's persistent state reads and writes). Here that state is, per stream b and KV head h, C
 slots of K and V plus a counter seq_len[b] of tokens ever appended. Token t
 lives in slot t mod C, so slot s holds token
     k(s) = L - 1 - ((L - 1 - s) mod C)       (L = seq_len, mod non-negative)
