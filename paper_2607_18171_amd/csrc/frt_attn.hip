@@ -138,6 +138,38 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
   const int c2 = oe > oa ? (oe - of + BN - 1) / BN : 0;
   const int T = c0 + c1 + c2;
 
+  const int c01 = c0 + c1;
+
+  // Tiles wholly visible to every row of the block, as absolute tile index
+  // ranges [fa_r, fb_r) per run; every other tile is masked. Keys of a run
+  // map to relative tokens key = slot - off (one physical run never wraps).
+  // A run holding slot hh strictly inside is the whole ring: it is fast only
+  // if every row sees every ring token.
+  const int klo = max(ilo, -lc), khi = min(ihi, -1);
+  auto fast_range = [&](int ra, int re, int rf, int off, int kl, int kh, int t0, int nt, int &fa,
+                        int &fb) __attribute__((always_inline)) {
+    const int lo_s = max(ra, kl + off), hi_s = min(re - 1, kh + off);
+    const int jmin = lo_s >= rf ? (lo_s - rf + BN - 1) / BN : 0;
+    const int num = hi_s + 1 - rf;
+    const int jend = num > 0 ? num / BN : 0;
+    const int a = min(jmin, nt), e = max(a, min(jend, nt));
+    fa = t0 + a;
+    fb = t0 + e;
+  };
+  int fa0 = 0, fb0 = 0, fa1 = 0, fb1 = 0, fa2 = 0, fb2 = 0;
+  if (c0 > 0) {
+    if (ra0 < hh && hh < re0) {
+      if (klo <= -C && khi >= -1) {
+        fa0 = 0;
+        fb0 = min(c0, (re0 - rf0) / BN);
+      }
+    } else {
+      fast_range(ra0, re0, rf0, ra0 < hh ? hh : hh + C, klo, khi, 0, c0, fa0, fb0);
+    }
+  }
+  if (c1 > 0) fast_range(ra1, re1, rf1, ra1 < hh ? hh : hh + C, klo, khi, c0, c1, fa1, fb1);
+  if (c2 > 0) fast_range(oa, oe, of, 0, ilo, ihi, c01, c2, fa2, fb2);
+
   const size_t head = (size_t)b * p.Hkv + kvh;
   const __amdgpu_buffer_rsrc_t rk_ring =
       make_rsrc(p.k_ring + head * (size_t)C * D, (uint32_t)((size_t)C * D * 2));
@@ -169,50 +201,46 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
   float m = 0.f, lsum = 0.f;
   bool mset = false;
 
-  // ---- tile bookkeeping (block-uniform, scalar) ----
-  // tile t -> run (0, 1: ring; 2: own) and first key (slot or own index)
-  auto tile_run = [&](int t) __attribute__((always_inline)) {
-    return t < c0 ? 0 : (t < c0 + c1 ? 1 : 2);
-  };
+  // ---- tile bookkeeping (block-uniform, scalar, branch free) ----
+  // tile t: first key (slot, or own index for t >= c01) and fast flag
+  const int dl0 = rf0, dl1 = rf1 - c0 * BN, dl2 = of - c01 * BN;
   auto tile_base = [&](int t) __attribute__((always_inline)) {
-    return t < c0 ? rf0 + t * BN : (t < c0 + c1 ? rf1 + (t - c0) * BN : of + (t - c0 - c1) * BN);
+    return t * BN + pick(t < c0, dl0, pick(t < c01, dl1, dl2));
   };
   auto tile_fast = [&](int t) __attribute__((always_inline)) {
-    const int run = tile_run(t), base = tile_base(t), end = base + BN;
-    if (run == 2) return base >= oa && end <= oe && base >= ilo && end - 1 <= ihi;
-    const int ra = pick(run == 0, ra0, ra1), re = pick(run == 0, re0, re1);
-    int kmin, kmax;
-    if (base < hh && hh < end) {
-      kmin = -C;
-      kmax = -1;
-    } else {
-      kmin = base < hh ? base - hh : base - hh - C;
-      kmax = (end - 1) < hh ? end - 1 - hh : end - 1 - hh - C;
-    }
-    return base >= ra && end <= re && end <= C && kmin >= max(ilo, -lc) && kmax <= ihi;
+    return (t >= fa0 && t < fb0) || (t >= fa1 && t < fb1) || (t >= fa2 && t < fb2);
   };
+
+  // per-thread parts of the staging offsets (bytes); the tile's first key is
+  // added per load, so the descriptors bound every access
+  uint32_t koff[KPT], voff_ring[VPT], voff_own[VPT];
+#pragma unroll
+  for (int u = 0; u < KPT; ++u) {
+    const int idx = tid + NT * u;
+    koff[u] = (uint32_t)(((idx / (D / 8)) * D + (idx % (D / 8)) * 8) * 2);
+  }
+#pragma unroll
+  for (int u = 0; u < VPT; ++u) {
+    const int idx = tid + NT * u;
+    const int dd = idx / (BN / 8), vc = idx % (BN / 8);
+    voff_ring[u] = (uint32_t)(((size_t)dd * C + vc * 8) * 2);
+    voff_own[u] = (uint32_t)(((size_t)dd * p.n_pad + vc * 8) * 2);
+  }
 
   u32x4 kreg[KPT], vreg[VPT];
   auto load_k = [&](int t) __attribute__((always_inline)) {
-    const int run = tile_run(t), base = tile_base(t);
-    const __amdgpu_buffer_rsrc_t rk = pick(run == 2, rk_own, rk_ring);
+    const bool own = t >= c01;
+    const __amdgpu_buffer_rsrc_t rk = pick(own, rk_own, rk_ring);
+    const uint32_t sb = (uint32_t)tile_base(t) * (uint32_t)(D * 2);
 #pragma unroll
-    for (int u = 0; u < KPT; ++u) {
-      const int idx = tid + NT * u;
-      const int kr = idx / (D / 8), kc = idx % (D / 8);
-      kreg[u] = buf_load16(rk, (uint32_t)(((size_t)(base + kr) * D + kc * 8) * 2));
-    }
+    for (int u = 0; u < KPT; ++u) kreg[u] = buf_load16(rk, koff[u] + sb);
   };
   auto load_v = [&](int t) __attribute__((always_inline)) {
-    const int run = tile_run(t), base = tile_base(t);
-    const __amdgpu_buffer_rsrc_t rv = pick(run == 2, rv_own, rv_ring);
-    const int vstride = pick(run == 2, p.n_pad, C);
+    const bool own = t >= c01;
+    const __amdgpu_buffer_rsrc_t rv = pick(own, rv_own, rv_ring);
+    const uint32_t sb = (uint32_t)tile_base(t) * 2u;
 #pragma unroll
-    for (int u = 0; u < VPT; ++u) {
-      const int idx = tid + NT * u;
-      const int dd = idx / (BN / 8), vc = idx % (BN / 8);
-      vreg[u] = buf_load16(rv, (uint32_t)(((size_t)dd * vstride + base + vc * 8) * 2));
-    }
+    for (int u = 0; u < VPT; ++u) vreg[u] = buf_load16(rv, pick(own, voff_own[u], voff_ring[u]) + sb);
   };
   auto store_k = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
@@ -247,16 +275,20 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
             *reinterpret_cast<const bf16x8 *>(krow + 16 * k), qf[k], s[kb], 0, 0, 0);
     }
   };
+  // row max over the tile: three-input max tree, then the lane 32 away
   auto row_max = [&](const f32x16 (&s)[2]) __attribute__((always_inline)) {
-    float mt = fmaxf(s[0][0], s[0][1]);
+    float mt = fmaxf(s[0][0], fmaxf(s[0][1], s[0][2]));
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; r += 2) mt = fmaxf(mt, fmaxf(s[kb][r], s[kb][r + 1]));
+    for (int i = 3; i < 31; i += 2) {
+      const float a = s[i >> 4][i & 15], c = s[(i + 1) >> 4][(i + 1) & 15];
+      mt = fmaxf(mt, fmaxf(a, c));
+    }
+    mt = fmaxf(mt, s[1][15]);
     return max_pair32(mt);
   };
   auto mask_tile = [&](int t, f32x16 (&s)[2]) __attribute__((always_inline)) {
-    const int run = tile_run(t), base = tile_base(t);
+    const int base = tile_base(t);
+    const int run = t < c0 ? 0 : (t < c01 ? 1 : 2);
     const int ra = pick(run == 0, ra0, pick(run == 1, ra1, oa));
     const int re = pick(run == 0, re0, pick(run == 1, re1, oe));
 #pragma unroll
@@ -325,8 +357,21 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
     bf16x8 pf[2][2];
     qk((t + 1) & 1, snext);
     softmax(scur, pf);
+    // QK(t+1) and softmax(t) are independent: interleave them
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // VALU
+    }
     pv(t & 1, pf);
     float mt = row_max(snext);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+      __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);  // VALU
+    }
     store_k(t & 1);
     store_v((t + 1) & 1);
     if (!tile_fast(t + 1)) {
