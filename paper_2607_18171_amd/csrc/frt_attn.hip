@@ -57,20 +57,28 @@ __device__ __forceinline__ float sum_pair32(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+typedef __attribute__((address_space(3))) void lds_void;
+
+// 16-byte HBM -> LDS load; lane i of the wave writes lds_base + 16*i
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off,
+                                      const void *lds_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)lds_base, 16, (int)byte_off, 0, 0, 0);
+}
+
 template <int D, int NW>
 __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
   constexpr int BN = kChunkBN;
   constexpr int BM = 32 * NW;
-  constexpr int NT = NW * 64;
-  constexpr int KST = D + 8;   // K tile row stride (elements)
-  constexpr int VST = BN + 8;  // V^T tile row stride (elements)
-  constexpr int KPT = BN * D / 8 / NT;
-  constexpr int VPT = D * BN / 8 / NT;
+  constexpr int CPR = D / 8;                  // 16-byte chunks per K row
+  constexpr int KDW = BN * CPR / 64 / NW;     // 1 KB LDS loads per wave per K tile
+  constexpr int VDW = D * (BN / 8) / 64 / NW;  // ... per V^T tile
   constexpr float kTau = 8.f;
   constexpr float kNegInf = -__builtin_inff();
-  static_assert(KPT >= 1 && VPT >= 1, "tile too small for the block");
-  __shared__ __attribute__((aligned(16))) uint16_t ks[2][BN * KST];
-  __shared__ __attribute__((aligned(16))) uint16_t vs[2][D * VST];
+  static_assert(BN == 64 && KDW >= 1 && VDW >= 1, "tile split");
+  __shared__ __attribute__((aligned(16))) uint16_t ks0[BN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t ks1[BN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t vs0[D * BN];
+  __shared__ __attribute__((aligned(16))) uint16_t vs1[D * BN];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, h = lane >> 5;
@@ -211,68 +219,71 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
     return (t >= fa0 && t < fb0) || (t >= fa1 && t < fb1) || (t >= fa2 && t < fb2);
   };
 
-  // per-thread parts of the staging offsets (bytes); the tile's first key is
-  // added per load, so the descriptors bound every access
-  uint32_t koff[KPT], voff_ring[VPT], voff_own[VPT];
+  // ---- tile loads: HBM -> LDS directly (no staging registers) ----
+  // One wave instruction writes 1 KB of consecutive LDS; the HBM chunk each
+  // lane fetches makes the LDS hold the tile XOR-swizzled, so that the MFMA
+  // fragment reads below are free of bank conflicts:
+  //   K tile:   LDS chunk (row, pc) holds key row `row`, d-chunk pc ^ (row % CPR)
+  //   V^T tile: LDS chunk (d, pc) holds row d, key chunk pc ^ ((d >> 1) & 7)
+  // Per-lane HBM offsets are fixed; the tile's first key is added per load, so
+  // the buffer descriptors bound every access.
+  uint32_t kdo[KDW], vdo_ring[VDW], vdo_own[VDW];
 #pragma unroll
-  for (int u = 0; u < KPT; ++u) {
-    const int idx = tid + NT * u;
-    koff[u] = (uint32_t)(((idx / (D / 8)) * D + (idx % (D / 8)) * 8) * 2);
+  for (int u = 0; u < KDW; ++u) {
+    const int pos = 64 * (wave * KDW + u) + lane;
+    const int row = pos / CPR, c = (pos % CPR) ^ (row % CPR);
+    kdo[u] = (uint32_t)((row * D + 8 * c) * 2);
   }
 #pragma unroll
-  for (int u = 0; u < VPT; ++u) {
-    const int idx = tid + NT * u;
-    const int dd = idx / (BN / 8), vc = idx % (BN / 8);
-    voff_ring[u] = (uint32_t)(((size_t)dd * C + vc * 8) * 2);
-    voff_own[u] = (uint32_t)(((size_t)dd * p.n_pad + vc * 8) * 2);
+  for (int u = 0; u < VDW; ++u) {
+    const int pos = 64 * (wave * VDW + u) + lane;
+    const int d = pos / 8, c = (pos % 8) ^ ((d >> 1) & 7);
+    vdo_ring[u] = (uint32_t)(((size_t)d * C + 8 * c) * 2);
+    vdo_own[u] = (uint32_t)(((size_t)d * p.n_pad + 8 * c) * 2);
   }
-
-  u32x4 kreg[KPT], vreg[VPT];
-  auto load_k = [&](int t) __attribute__((always_inline)) {
+  auto dma_k = [&](int t, uint16_t *kb) __attribute__((always_inline)) {
     const bool own = t >= c01;
     const __amdgpu_buffer_rsrc_t rk = pick(own, rk_own, rk_ring);
     const uint32_t sb = (uint32_t)tile_base(t) * (uint32_t)(D * 2);
 #pragma unroll
-    for (int u = 0; u < KPT; ++u) kreg[u] = buf_load16(rk, koff[u] + sb);
+    for (int u = 0; u < KDW; ++u) dma16(rk, kdo[u] + sb, kb + 512 * (wave * KDW + u));
   };
-  auto load_v = [&](int t) __attribute__((always_inline)) {
+  auto dma_v = [&](int t, uint16_t *vb) __attribute__((always_inline)) {
     const bool own = t >= c01;
     const __amdgpu_buffer_rsrc_t rv = pick(own, rv_own, rv_ring);
     const uint32_t sb = (uint32_t)tile_base(t) * 2u;
 #pragma unroll
-    for (int u = 0; u < VPT; ++u) vreg[u] = buf_load16(rv, pick(own, voff_own[u], voff_ring[u]) + sb);
+    for (int u = 0; u < VDW; ++u)
+      dma16(rv, pick(own, vdo_own[u], vdo_ring[u]) + sb, vb + 512 * (wave * VDW + u));
   };
-  auto store_k = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-    for (int u = 0; u < KPT; ++u) {
-      const int idx = tid + NT * u;
-      const int kr = idx / (D / 8), kc = idx % (D / 8);
-      *reinterpret_cast<u32x4 *>(&ks[buf][kr * KST + kc * 8]) = kreg[u];
-    }
-  };
-  auto store_v = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-    for (int u = 0; u < VPT; ++u) {
-      const int idx = tid + NT * u;
-      const int dd = idx / (BN / 8), vc = idx % (BN / 8);
-      *reinterpret_cast<u32x4 *>(&vs[buf][dd * VST + vc * 8]) = vreg[u];
-    }
+  // all of this thread's tile loads have landed in LDS
+  auto wait_dma = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
   };
 
   // ---- per-wave compute pieces ----
   const int prow = perm23(l32);
-  // S^T for the 64 keys of K buffer kbuf
-  auto qk = [&](int kbuf, f32x16 (&s)[2]) __attribute__((always_inline)) {
+  // per-lane element offsets of the MFMA fragments inside a (swizzled) tile
+  int kfo[D / 16];
+#pragma unroll
+  for (int k = 0; k < D / 16; ++k) kfo[k] = (prow * CPR + ((2 * k + h) ^ (prow % CPR))) * 8;
+  int vfo[2][2];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) vfo[kb][j] = (l32 * 8 + ((4 * kb + 2 * j + h) ^ ((l32 >> 1) & 7))) * 8;
+  // S^T for the 64 keys of a K buffer
+  auto qk = [&](const uint16_t *kt, f32x16 (&s)[2]) __attribute__((always_inline)) {
     const f32x16 zero = {};
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      const uint16_t *krow = &ks[kbuf][(32 * kb + prow) * KST + 8 * h];
+      const uint16_t *kblk = kt + kb * 32 * D;
       s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-          *reinterpret_cast<const bf16x8 *>(krow), qf[0], zero, 0, 0, 0);
+          *reinterpret_cast<const bf16x8 *>(kblk + kfo[0]), qf[0], zero, 0, 0, 0);
 #pragma unroll
       for (int k = 1; k < D / 16; ++k)
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            *reinterpret_cast<const bf16x8 *>(krow + 16 * k), qf[k], s[kb], 0, 0, 0);
+            *reinterpret_cast<const bf16x8 *>(kblk + kfo[k]), qf[k], s[kb], 0, 0, 0);
     }
   };
   // row max over the tile: three-input max tree, then the lane 32 away
@@ -336,26 +347,29 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
           lsum = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, lsum, false);
         }
   };
-  auto pv = [&](int vbuf, const bf16x8 (&pf)[2][2]) __attribute__((always_inline)) {
+  // O^T += V^T P^T for the 64 keys of a V^T buffer
+  auto pv = [&](const uint16_t *vt, const bf16x8 (&pf)[2][2]) __attribute__((always_inline)) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
-        const uint16_t *vrow = &vs[vbuf][(32 * db + l32) * VST + 8 * h + 32 * kb];
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8 *>(vrow),
-                                                        pf[kb][0], o[db], 0, 0, 0);
+        const uint16_t *vblk = vt + db * 32 * BN;
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            *reinterpret_cast<const bf16x8 *>(vrow + 16), pf[kb][1], o[db], 0, 0, 0);
+            *reinterpret_cast<const bf16x8 *>(vblk + vfo[kb][0]), pf[kb][0], o[db], 0, 0, 0);
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            *reinterpret_cast<const bf16x8 *>(vblk + vfo[kb][1]), pf[kb][1], o[db], 0, 0, 0);
       }
   };
 
-  // One pipelined iteration for a tile t that has a successor: QK(t+1) with
-  // softmax(t), PV(t) with max(t+1); stage K(t+2) and V(t+1) into LDS.
-  auto step = [&](int t, f32x16 (&scur)[2], f32x16 (&snext)[2]) __attribute__((always_inline)) {
-    load_k(min(t + 2, T - 1));
-    load_v(t + 1);
+  // One pipelined iteration for a tile t that has a successor (par = t & 1):
+  // QK(t+1) with softmax(t), PV(t) with max(t+1); K(t+2) and V(t+1) land in
+  // the buffers tile t and tile t-1 left free.
+  auto step = [&](int t, const int par, f32x16 (&scur)[2], f32x16 (&snext)[2])
+                  __attribute__((always_inline)) {
+    dma_k(min(t + 2, T - 1), par ? ks1 : ks0);
+    dma_v(t + 1, par ? vs0 : vs1);
     bf16x8 pf[2][2];
-    qk((t + 1) & 1, snext);
+    qk(par ? ks0 : ks1, snext);
     softmax(scur, pf);
     // QK(t+1) and softmax(t) are independent: interleave them
 #pragma unroll
@@ -364,7 +378,7 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
       __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // VALU
     }
-    pv(t & 1, pf);
+    pv(par ? vs1 : vs0, pf);
     float mt = row_max(snext);
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
@@ -372,45 +386,40 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
       __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);  // VALU
     }
-    store_k(t & 1);
-    store_v((t + 1) & 1);
     if (!tile_fast(t + 1)) {
       mask_tile(t + 1, snext);
       mt = row_max(snext);
     }
     rescale(mt);
+    wait_dma();
     __syncthreads();
   };
 
   f32x16 sa[2], sb[2];
   if (T > 0) {
-    load_k(0);
-    load_v(0);
-    store_k(0);
-    store_v(0);
-    if (T > 1) {
-      load_k(1);
-      store_k(1);
-    }
+    dma_k(0, ks0);
+    dma_v(0, vs0);
+    dma_k(min(1, T - 1), ks1);
+    wait_dma();
     __syncthreads();
-    qk(0, sa);
+    qk(ks0, sa);
     if (!tile_fast(0)) mask_tile(0, sa);
     rescale(row_max(sa));
     __syncthreads();  // K buffer 0 is refilled by the first step
 
     int t = 0;
     for (; t + 2 < T; t += 2) {
-      step(t, sa, sb);
-      step(t + 1, sb, sa);
+      step(t, 0, sa, sb);
+      step(t + 1, 1, sb, sa);
     }
     bf16x8 pf[2][2];
-    if (t + 1 < T) {  // two tiles left
-      step(t, sa, sb);
+    if (t + 1 < T) {  // two tiles left (t is even)
+      step(t, 0, sa, sb);
       softmax(sb, pf);
-      pv((t + 1) & 1, pf);
+      pv(vs1, pf);
     } else {  // one tile left
       softmax(sa, pf);
-      pv(t & 1, pf);
+      pv(vs0, pf);
     }
   }
 
