@@ -80,7 +80,8 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
   __shared__ __attribute__((aligned(16))) uint16_t vs0[D * BN];
   __shared__ __attribute__((aligned(16))) uint16_t vs1[D * BN];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // scalar: LDS load bases in M0
   const int l32 = lane & 31, h = lane >> 5;
 
   // Blocks are dealt to the 8 XCDs round robin; give each XCD a contiguous
@@ -242,6 +243,7 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
     vdo_own[u] = (uint32_t)(((size_t)d * p.n_pad + 8 * c) * 2);
   }
   auto dma_k = [&](int t, uint16_t *kb) __attribute__((always_inline)) {
+    t = __builtin_amdgcn_readfirstlane(t);  // uniform: the descriptor stays scalar
     const bool own = t >= c01;
     const __amdgpu_buffer_rsrc_t rk = pick(own, rk_own, rk_ring);
     const uint32_t sb = (uint32_t)tile_base(t) * (uint32_t)(D * 2);
@@ -249,6 +251,7 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
     for (int u = 0; u < KDW; ++u) dma16(rk, kdo[u] + sb, kb + 512 * (wave * KDW + u));
   };
   auto dma_v = [&](int t, uint16_t *vb) __attribute__((always_inline)) {
+    t = __builtin_amdgcn_readfirstlane(t);
     const bool own = t >= c01;
     const __amdgpu_buffer_rsrc_t rv = pick(own, rv_own, rv_ring);
     const uint32_t sb = (uint32_t)tile_base(t) * 2u;
@@ -297,19 +300,26 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
     mt = fmaxf(mt, s[1][15]);
     return max_pair32(mt);
   };
+  // Mask of an edge tile, branch free. Key (slot or own index) sl is visible to
+  // this lane's row iff it lies in the tile's run and its token, relative to
+  // L, lies in [vlo, vhi]; ring slots at or after hh hold tokens one ring
+  // length further back.
   auto mask_tile = [&](int t, f32x16 (&s)[2]) __attribute__((always_inline)) {
     const int base = tile_base(t);
-    const int run = t < c0 ? 0 : (t < c01 ? 1 : 2);
-    const int ra = pick(run == 0, ra0, pick(run == 1, ra1, oa));
-    const int re = pick(run == 0, re0, pick(run == 1, re1, oe));
+    const bool own = t >= c01, r0 = t < c0;
+    const int ra = pick(r0, ra0, pick(own, oa, ra1));
+    const int re = pick(r0, re0, pick(own, oe, re1));
+    const int kbase = own ? 0 : hh;
+    const int hsplit = own ? 0x7fffffff : hh;
+    const uint32_t rspan = (uint32_t)(re - ra);
+    const uint32_t vspan = (uint32_t)(vhi - vlo);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int sl = base + 32 * kb + 16 * (r >> 3) + 8 * h + (r & 7);
-        const int krel = run == 2 ? sl : (sl < hh ? sl - hh : sl - hh - C);
-        const bool ok = sl >= ra && sl < re && (run == 2 || (sl < C && krel >= -lc)) &&
-                        krel >= vlo && krel <= vhi;
+        const int krel = sl - kbase - (sl >= hsplit ? C : 0);
+        const bool ok = ((uint32_t)(sl - ra) < rspan) & ((uint32_t)(krel - vlo) <= vspan);
         s[kb][r] = ok ? s[kb][r] : kNegInf;
       }
   };
