@@ -386,7 +386,7 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
     for (int i = 0; i < 16; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
-      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // VALU
+      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // VALU
     }
     pv(par ? vs1 : vs0, pf);
     float mt = row_max(snext);
