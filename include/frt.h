@@ -192,14 +192,15 @@ frt_status frt_stream_attn_step(const frt_ring *ring, const frt_rope *rope,
 int32_t frt_decode_max_splits(const frt_ring *ring);
 
 /* Workspace bytes frt_decode_attn needs: fp32 partial (max, sum, output)
- * per stream, KV head, split and query head. */
+ * per stream, KV head and query head, for every split plus one holding the
+ * step's own token. */
 size_t frt_decode_workspace_bytes(const frt_ring *ring, int32_t num_q_heads);
 
 /*
  * One-token decode step for every stream: frt_stream_attn_step with
- * n_new = 1, computed as split-KV (each split of 256 ring slots yields a
- * partial max/sum/output per query head) followed by a combine pass that
- * also adds the own token. Same tensor layouts with n_new = 1.
+ * n_new = 1, computed as split-KV (each split of 256 ring slots, and the own
+ * token on its own, yields a partial max/sum/output per query head) followed
+ * by a combine pass. Same tensor layouts with n_new = 1.
  * num_q_heads / num_kv_heads must be <= 16.
  */
 frt_status frt_decode_attn(const frt_ring *ring, const frt_rope *rope,

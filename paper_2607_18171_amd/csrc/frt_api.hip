@@ -267,6 +267,8 @@ frt_status frt_kv_append(const frt_ring *ring, const frt_rope *rope, const void 
   p.n = n_new;
   const RopeDev rd = rope_dev(rope);
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if (n_new <= kAppendSmall)  // one block per stream, seq_len advanced in the same launch
+    return launch("rope_append", st, [&] { return launch_rope_append_small(p, rd, st); });
   if ((s = launch("rope_append", st, [&] { return launch_rope_append(p, rd, st); })) != FRT_OK)
     return s;
   return launch("seq_advance", st, [&] { return launch_seq_advance(ring->seq_len, p.B, n_new, st); });
@@ -360,7 +362,8 @@ int32_t frt_decode_max_splits(const frt_ring *ring) {
 size_t frt_decode_workspace_bytes(const frt_ring *ring, int32_t num_q_heads) {
   if (!ring || ring->num_kv_heads <= 0 || num_q_heads <= 0 || ring->head_dim <= 0) return 0;
   const int G = num_q_heads / ring->num_kv_heads;
-  return (size_t)ring->num_streams * ring->num_kv_heads * frt_decode_max_splits(ring) *
+  // one partial per split plus one for the step's own token
+  return (size_t)ring->num_streams * ring->num_kv_heads * (frt_decode_max_splits(ring) + 1) *
          decode_split_floats(G, ring->head_dim) * sizeof(float);
 }
 
@@ -413,7 +416,7 @@ frt_status frt_decode_attn(const frt_ring *ring, const frt_rope *rope, const frt
   hipStream_t st = static_cast<hipStream_t>(stream);
   if ((s = launch("decode_split", st, [&] { return launch_decode_split(p, rd, st); })) != FRT_OK)
     return s;
-  return launch("decode_combine", st, [&] { return launch_decode_combine(p, rd, st); });
+  return launch("decode_combine", st, [&] { return launch_decode_combine(p, st); });
 }
 
 frt_status frt_timing_enable(int32_t on) {

@@ -51,6 +51,40 @@ __global__ __launch_bounds__(256) void rope_append_kernel(AppendParams p, RopeDe
   }
 }
 
+// Appends of a few tokens (n <= kAppendSmall, e.g. one decode token): one
+// block per stream writes the slots of every KV head and then advances
+// seq_len itself, once all of its threads are past their reads of it.
+template <int D>
+__global__ __launch_bounds__(256) void rope_append_small_kernel(AppendParams p, RopeDev rope) {
+  constexpr int CH = D / 8;  // 16-byte chunks per row
+  const RopeReg rg = rope_reg(rope);
+  const int b = blockIdx.x;
+  const long long L = p.seq_len[b];
+  const int total = p.n * p.Hkv * CH;
+  for (int idx = threadIdx.x; idx < total; idx += 256) {
+    const int c = idx % CH, rest = idx / CH;
+    const int kvh = rest % p.Hkv, i = rest / p.Hkv;
+    const size_t src = (((size_t)b * p.n + i) * p.Hkv + kvh) * D + c * 8;
+    const long long pos = L + i;
+    int co[3];
+    rope_coords(rg, pos, co);
+    const u32x4 y = rotate8_round(rg, co, c * 4, *reinterpret_cast<const u32x4 *>(p.k_new + src),
+                                  1.0);
+    const long long slot = pos % p.C;
+    const size_t head = (size_t)b * p.Hkv + kvh;
+    *reinterpret_cast<u32x4 *>(p.k_ring + (head * p.C + slot) * D + c * 8) = y;
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(p.v_new + src);
+    uint16_t *vd = p.v_ring + (head * D + c * 8) * (size_t)p.C + slot;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      vd[(size_t)(2 * w) * p.C] = (uint16_t)(v[w] & 0xFFFFu);
+      vd[(size_t)(2 * w + 1) * p.C] = (uint16_t)(v[w] >> 16);
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) p.seq_len[b] = L + p.n;
+}
+
 __global__ void seq_advance_kernel(int64_t *seq_len, int B, int n) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b < B) seq_len[b] += n;
@@ -122,6 +156,14 @@ hipError_t launch_rope_append(const AppendParams &p, const RopeDev &r, hipStream
     hipLaunchKernelGGL(rope_append_kernel<128>, grid, dim3(256), 0, s, p, r);
   else
     hipLaunchKernelGGL(rope_append_kernel<64>, grid, dim3(256), 0, s, p, r);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_append_small(const AppendParams &p, const RopeDev &r, hipStream_t s) {
+  if (p.D == 128)
+    hipLaunchKernelGGL(rope_append_small_kernel<128>, dim3(p.B), dim3(256), 0, s, p, r);
+  else
+    hipLaunchKernelGGL(rope_append_small_kernel<64>, dim3(p.B), dim3(256), 0, s, p, r);
   return hipGetLastError();
 }
 

@@ -39,6 +39,13 @@ __device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t b
   return __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 0);
 }
 
+// Two packed bf16 values as a vector. Taking the word by value matters:
+// __builtin_bit_cast applied directly to a subscripted vector element has
+// been seen to read element 0 whatever the index.
+__device__ __forceinline__ bf16x2 u32_as_bf16x2(uint32_t w) {
+  return __builtin_bit_cast(bf16x2, w);
+}
+
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) {
   return __uint_as_float(b << 16);
 }

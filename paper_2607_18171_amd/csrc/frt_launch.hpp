@@ -46,7 +46,7 @@ struct DecodeParams {
   const uint16_t *v_new;   // [B][1][Hkv][D]
   const uint16_t *k_ring, *v_ring;
   const int64_t *seq_len;
-  float *ws;               // partials, see decode_ws_floats
+  float *ws;               // partials: (nsplit + 1) per (stream, KV head)
   uint16_t *out;           // [B][1][Hq][D]
   float *lse;              // [B][Hq][1] or null
   int B, Hq, Hkv, G, D, C, nsplit;
@@ -55,6 +55,7 @@ struct DecodeParams {
 };
 
 constexpr int kAppendTokens = 64;   // tokens per append / prep block
+constexpr int kAppendSmall = 16;    // appends up to this many tokens take one launch
 constexpr int kChunkBN = 64;        // keys per attention tile
 #ifndef FRT_ATTN_WAVES
 #define FRT_ATTN_WAVES 8
@@ -67,10 +68,11 @@ constexpr int kDecodeSplit = 256;   // ring slots per decode split
 __host__ __device__ inline size_t decode_split_floats(int G, int D) { return (size_t)G * (2 + D); }
 
 hipError_t launch_rope_append(const AppendParams &p, const RopeDev &r, hipStream_t s);
+hipError_t launch_rope_append_small(const AppendParams &p, const RopeDev &r, hipStream_t s);
 hipError_t launch_seq_advance(int64_t *seq_len, int B, int n, hipStream_t s);
 hipError_t launch_chunk_prep(const PrepParams &p, const RopeDev &r, hipStream_t s);
 hipError_t launch_chunk_attn(const AttnParams &p, int D, hipStream_t s);
 hipError_t launch_decode_split(const DecodeParams &p, const RopeDev &r, hipStream_t s);
-hipError_t launch_decode_combine(const DecodeParams &p, const RopeDev &r, hipStream_t s);
+hipError_t launch_decode_combine(const DecodeParams &p, hipStream_t s);
 
 }  // namespace frt

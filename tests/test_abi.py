@@ -110,7 +110,7 @@ def test_decode_rejects_bad_arguments():
     o = rope()
     wsb = lib.frt_decode_workspace_bytes(ctypes.byref(r), 8)
     assert lib.frt_decode_max_splits(ctypes.byref(r)) == 1
-    assert wsb == 1 * 1 * 1 * 8 * (2 + 128) * 4
+    assert wsb == 1 * 1 * (1 + 1) * 8 * (2 + 128) * 4  # one split + the own-token partial
 
     def dec(hq=8, ws=FAKE, n=wsb):
         return lib.frt_decode_attn(ctypes.byref(r), ctypes.byref(o), ctypes.byref(m), FAKE, FAKE,
