@@ -188,19 +188,23 @@ frt_status frt_stream_attn_step(const frt_ring *ring, const frt_rope *rope,
                                 size_t workspace_bytes, void *out, float *lse,
                                 void *hip_stream);
 
-/* Largest number of KV splits a decode call uses (ceil(capacity / 256)). */
+/* Largest number of KV pieces a decode call splits the ring into (one
+ * partial each): every (stream, KV head) is cut into pieces of consecutive
+ * 32-token tiles, sized on the device so that the pieces spread evenly over
+ * the waves that run at once. Depends on num_streams, num_kv_heads and
+ * capacity only. */
 int32_t frt_decode_max_splits(const frt_ring *ring);
 
-/* Workspace bytes frt_decode_attn needs: fp32 partial (max, sum, output)
- * per stream, KV head and query head, for every split plus one holding the
- * step's own token. */
+/* Workspace bytes frt_decode_attn needs: an fp32 partial (max, sum, output
+ * per query head of the group) for each of frt_decode_max_splits pieces and
+ * one per (stream, KV head) holding the step's own token. */
 size_t frt_decode_workspace_bytes(const frt_ring *ring, int32_t num_q_heads);
 
 /*
  * One-token decode step for every stream: frt_stream_attn_step with
- * n_new = 1, computed as split-KV (each split of 256 ring slots, and the own
- * token on its own, yields a partial max/sum/output per query head) followed
- * by a combine pass. Same tensor layouts with n_new = 1.
+ * n_new = 1, computed as split-KV (each piece of the visible ring tokens, and
+ * the own token on its own, yields a partial max/sum/output per query head)
+ * followed by a combine pass. Same tensor layouts with n_new = 1.
  * num_q_heads / num_kv_heads must be <= 16.
  */
 frt_status frt_decode_attn(const frt_ring *ring, const frt_rope *rope,

@@ -355,16 +355,17 @@ frt_status frt_stream_attn_step(const frt_ring *ring, const frt_rope *rope, cons
 }
 
 int32_t frt_decode_max_splits(const frt_ring *ring) {
-  if (!ring || ring->capacity <= 0) return 0;
-  return (ring->capacity + kDecodeSplit - 1) / kDecodeSplit;
+  if (!ring || ring->capacity <= 0 || ring->num_streams <= 0 || ring->num_kv_heads <= 0) return 0;
+  return decode_piece_waves(ring->num_streams, ring->num_kv_heads, ring->capacity);
 }
 
 size_t frt_decode_workspace_bytes(const frt_ring *ring, int32_t num_q_heads) {
   if (!ring || ring->num_kv_heads <= 0 || num_q_heads <= 0 || ring->head_dim <= 0) return 0;
   const int G = num_q_heads / ring->num_kv_heads;
-  // one partial per split plus one for the step's own token
-  return (size_t)ring->num_streams * ring->num_kv_heads * (frt_decode_max_splits(ring) + 1) *
-         decode_split_floats(G, ring->head_dim) * sizeof(float);
+  // a partial per piece wave, and one per (stream, KV head) for its own token
+  const size_t heads = (size_t)ring->num_streams * ring->num_kv_heads;
+  return ((size_t)frt_decode_max_splits(ring) + heads) * decode_split_floats(G, ring->head_dim) *
+         sizeof(float);
 }
 
 frt_status frt_decode_attn(const frt_ring *ring, const frt_rope *rope, const frt_mask *mask,
@@ -407,7 +408,7 @@ frt_status frt_decode_attn(const frt_ring *ring, const frt_rope *rope, const frt
   p.G = G;
   p.D = ring->head_dim;
   p.C = ring->capacity;
-  p.nsplit = frt_decode_max_splits(ring);
+  p.nwaves = frt_decode_max_splits(ring);
   p.mask_kind = mask->kind;
   p.mask_block = mask->block;
   p.mask_window = mask->window;

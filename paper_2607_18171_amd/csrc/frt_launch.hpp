@@ -46,10 +46,11 @@ struct DecodeParams {
   const uint16_t *v_new;   // [B][1][Hkv][D]
   const uint16_t *k_ring, *v_ring;
   const int64_t *seq_len;
-  float *ws;               // partials: (nsplit + 1) per (stream, KV head)
+  float *ws;               // partials: nwaves + B * Hkv
   uint16_t *out;           // [B][1][Hq][D]
   float *lse;              // [B][Hq][1] or null
-  int B, Hq, Hkv, G, D, C, nsplit;
+  int B, Hq, Hkv, G, D, C;
+  int nwaves;              // piece waves of the split pass (multiple of 4)
   int mask_kind, mask_block, mask_window;
   double qmul;
 };
@@ -62,9 +63,21 @@ constexpr int kChunkBN = 64;        // keys per attention tile
 #endif
 constexpr int kChunkWaves = FRT_ATTN_WAVES;  // waves per attention block
 constexpr int kChunkRows = 32 * kChunkWaves;  // query rows per block (32 per wave)
-constexpr int kDecodeSplit = 256;   // ring slots per decode split
+constexpr int kDecResident = 2048;  // decode split waves resident at once (2 per SIMD)
+constexpr int kDecChunk = 12;       // most 32-token tiles of one decode piece
 
-// Floats of decode workspace per (stream, kv head, split): max[G], sum[G], out[G][D].
+// Floats of one decode partial: max[G], sum[G], out[G][D].
+// Piece waves of a decode call: enough for every split of the tiles
+// (resident waves plus one per head, or pieces of kDecChunk tiles when the
+// ring is long), rounded up to whole blocks of 4 waves.
+__host__ __device__ inline int decode_piece_waves(int B, int Hkv, int C) {
+  const long long heads = (long long)B * Hkv;
+  const long long tiles_max = (long long)C / 32 + 1;
+  const long long cap = heads * ((tiles_max + kDecChunk - 1) / kDecChunk) + heads;
+  long long w = kDecResident + heads;
+  w = w > cap ? w : cap;
+  return (int)((w + 3) / 4 * 4);
+}
 __host__ __device__ inline size_t decode_split_floats(int G, int D) { return (size_t)G * (2 + D); }
 
 hipError_t launch_rope_append(const AppendParams &p, const RopeDev &r, hipStream_t s);

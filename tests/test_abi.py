@@ -109,8 +109,11 @@ def test_decode_rejects_bad_arguments():
     m = B.CMask(B.MASK_CAUSAL, 0, 0)
     o = rope()
     wsb = lib.frt_decode_workspace_bytes(ctypes.byref(r), 8)
-    assert lib.frt_decode_max_splits(ctypes.byref(r)) == 1
-    assert wsb == 1 * 1 * (1 + 1) * 8 * (2 + 128) * 4  # one split + the own-token partial
+    # piece waves: the resident count (2048) plus one per (stream, KV head),
+    # rounded up to blocks of 4; the workspace adds one own-token partial per head
+    waves = lib.frt_decode_max_splits(ctypes.byref(r))
+    assert waves == (2048 + 1 + 3) // 4 * 4
+    assert wsb == (waves + 1) * 8 * (2 + 128) * 4
 
     def dec(hq=8, ws=FAKE, n=wsb):
         return lib.frt_decode_attn(ctypes.byref(r), ctypes.byref(o), ctypes.byref(m), FAKE, FAKE,
