@@ -75,7 +75,12 @@ enum { FRT_MASK_BLOCK_CAUSAL = 1, FRT_MASK_CAUSAL = 2 };
  * tokens ever appended to stream b; the tokens still held are
  * [max(0, seq_len-capacity), seq_len).
  *   k_ring : bf16 [num_streams][num_kv_heads][capacity][head_dim]   (row per slot)
- *   v_ring : bf16 [num_streams][num_kv_heads][head_dim][capacity]   (slot-contiguous)
+ *   v_ring : bf16 [num_streams][num_kv_heads][capacity*head_dim] in blocks of
+ *            32 slots: block k (slots 32k ..) starts at element 32*head_dim*k of
+ *            the head and holds its slots row by row of the head dimension, so
+ *            (slot s, dim d) is element 32*head_dim*(s/32) + w*d + s%32, where
+ *            w = 32 for a full block and w = capacity%32 for a partial last one.
+ *            The 32 keys of one block are one contiguous 64*head_dim-byte run.
  *   seq_len: int64 [num_streams], device memory.
  * head_dim is 64 or 128; capacity is a positive multiple of 8. A new ring
  * must be zero-filled with seq_len = 0 (slot contents must stay finite:

@@ -116,10 +116,27 @@ def _stream(stream) -> Optional[int]:
 
 
 # ------------------------------------------------------------------ state --
+V_BLOCK = 32  # slots per V ring block
+
+
+def v_offsets(capacity: int, head_dim: int):
+    """Element offset of (slot, dim) inside one head's V ring storage, as an
+    int64 tensor [capacity][head_dim]: blocks of V_BLOCK slots, each stored row
+    by row of the head dimension (a partial last block has rows of
+    capacity % V_BLOCK slots)."""
+    import torch
+    s = torch.arange(capacity, dtype=torch.int64)[:, None]
+    d = torch.arange(head_dim, dtype=torch.int64)[None, :]
+    nfull = capacity // V_BLOCK
+    w = torch.where(s // V_BLOCK < nfull, V_BLOCK, capacity - V_BLOCK * nfull)
+    return V_BLOCK * head_dim * (s // V_BLOCK) + w * d + s % V_BLOCK
+
+
 class Ring:
     """A ring-buffer KV cache in device memory (torch tensors), zero-filled.
 
-    k: bf16 [B][Hkv][C][d]; v: bf16 [B][Hkv][d][C] (slot-contiguous); seq_len: int64 [B].
+    k: bf16 [B][Hkv][C][d]; v: bf16 [B][Hkv][C*d] in blocks of V_BLOCK slots
+    (element of slot s, dim d: v_offsets(C, d)[s, d]); seq_len: int64 [B].
     """
 
     def __init__(self, num_streams: int, num_kv_heads: int, head_dim: int, capacity: int,
@@ -129,13 +146,26 @@ class Ring:
         self.k = k if k is not None else torch.zeros(
             (num_streams, num_kv_heads, capacity, head_dim), dtype=torch.bfloat16, device=device)
         self.v = v if v is not None else torch.zeros(
-            (num_streams, num_kv_heads, head_dim, capacity), dtype=torch.bfloat16, device=device)
+            (num_streams, num_kv_heads, capacity * head_dim), dtype=torch.bfloat16, device=device)
         self.seq_len = seq_len if seq_len is not None else torch.zeros(
             num_streams, dtype=torch.int64, device=device)
 
     def c(self) -> CRing:
         return CRing(self.B, self.Hkv, self.d, self.C, _ptr(self.k), _ptr(self.v),
                      _ptr(self.seq_len))
+
+    def v_index(self, slots=None):
+        """Flat element indices into a head's V storage for `slots` (all
+        slots when None), shaped [len(slots)][d], on the ring's device."""
+        off = v_offsets(self.C, self.d)
+        if slots is not None:
+            off = off[slots]
+        return off.to(self.v.device)
+
+    def v_tokens(self):
+        """V as bf16 [B][Hkv][C][d] (slot-major copy of the block layout)."""
+        idx = self.v_index()
+        return self.v[:, :, idx.reshape(-1)].reshape(self.B, self.Hkv, self.C, self.d)
 
     def view_stream(self, b: int) -> "Ring":
         """A one-stream view sharing memory with stream b."""

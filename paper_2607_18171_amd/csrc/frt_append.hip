@@ -4,7 +4,8 @@
 // Both kernels are HBM-bound copies with a rotation in double precision: each
 // block owns 64 consecutive tokens of one (stream, KV head); rows are read and
 // written as 16-byte vectors, and V is transposed through LDS so that the
-// slot-contiguous V ring is written with consecutive lanes on consecutive slots.
+// block layout of the V ring is written with consecutive lanes on consecutive
+// slots.
 #include "frt_launch.hpp"
 
 namespace frt {
@@ -45,9 +46,10 @@ __global__ __launch_bounds__(256) void rope_append_kernel(AppendParams p, RopeDe
   __syncthreads();
   const int r = threadIdx.x & 63;
   if (r < ntok) {
-    const long long slot = (L + t0 + r) % p.C;
-    uint16_t *vdst = p.v_ring + head * (size_t)D * p.C + slot;
-    for (int dd = threadIdx.x >> 6; dd < D; dd += 4) vdst[(size_t)dd * p.C] = vs[r * VS + dd];
+    const int slot = (int)((L + t0 + r) % p.C);
+    uint16_t *vdst = p.v_ring + head * (size_t)D * p.C + vring_elem(slot, 0, p.C, D);
+    const uint32_t w = vring_width(slot, p.C);
+    for (int dd = threadIdx.x >> 6; dd < D; dd += 4) vdst[dd * w] = vs[r * VS + dd];
   }
 }
 
@@ -74,11 +76,12 @@ __global__ __launch_bounds__(256) void rope_append_small_kernel(AppendParams p, 
     const size_t head = (size_t)b * p.Hkv + kvh;
     *reinterpret_cast<u32x4 *>(p.k_ring + (head * p.C + slot) * D + c * 8) = y;
     const u32x4 v = *reinterpret_cast<const u32x4 *>(p.v_new + src);
-    uint16_t *vd = p.v_ring + (head * D + c * 8) * (size_t)p.C + slot;
+    uint16_t *vd = p.v_ring + head * (size_t)D * p.C + vring_elem((int)slot, c * 8, p.C, D);
+    const uint32_t vw = vring_width((int)slot, p.C);
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
-      vd[(size_t)(2 * w) * p.C] = (uint16_t)(v[w] & 0xFFFFu);
-      vd[(size_t)(2 * w + 1) * p.C] = (uint16_t)(v[w] >> 16);
+      vd[(2 * w) * vw] = (uint16_t)(v[w] & 0xFFFFu);
+      vd[(2 * w + 1) * vw] = (uint16_t)(v[w] >> 16);
     }
   }
   __syncthreads();
@@ -137,13 +140,16 @@ __global__ __launch_bounds__(256) void chunk_prep_kernel(PrepParams p, RopeDev r
   }
   __syncthreads();
 
-  // transposed values: token pairs (2 per thread) x D rows
+  // values in the V ring's block layout (n_pad is a multiple of the block, so
+  // every block is full): token pairs (2 per thread) x D rows
   if (t0 < p.n_pad) {
     const int ip = threadIdx.x & 31;
-    uint16_t *vbase = p.vt + head * (size_t)D * p.n_pad + t0 + 2 * ip;
+    const int s = t0 + 2 * ip;
+    uint16_t *vbase = p.vt + head * (size_t)D * p.n_pad + (size_t)(s / kVBlock) * kVBlock * D +
+                      s % kVBlock;
     for (int dd = threadIdx.x >> 5; dd < D; dd += 8) {
       const uint32_t lo = vs[(2 * ip) * VS + dd], hi = vs[(2 * ip + 1) * VS + dd];
-      *reinterpret_cast<uint32_t *>(vbase + (size_t)dd * p.n_pad) = lo | (hi << 16);
+      *reinterpret_cast<uint32_t *>(vbase + dd * kVBlock) = lo | (hi << 16);
     }
   }
 }

@@ -228,20 +228,31 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
   //   V^T tile: LDS chunk (d, pc) holds row d, key chunk pc ^ ((d >> 1) & 7)
   // Per-lane HBM offsets are fixed; the tile's first key is added per load, so
   // the buffer descriptors bound every access.
-  uint32_t kdo[KDW], vdo_ring[VDW], vdo_own[VDW];
+  // V (ring and own chunk alike) is stored in blocks of kVBlock keys, row d
+  // of a block contiguous; a tile starts on a block boundary, so a lane's
+  // chunk (d, c) sits at a fixed offset from the tile's first block. Only a
+  // partial last ring block (C not a multiple of the block) breaks that.
+  static_assert(BN % kVBlock == 0, "tiles start on V block boundaries");
+  uint32_t kdo[KDW], vdo[VDW];
 #pragma unroll
   for (int u = 0; u < KDW; ++u) {
     const int pos = 64 * (wave * KDW + u) + lane;
     const int row = pos / CPR, c = (pos % CPR) ^ (row % CPR);
     kdo[u] = (uint32_t)((row * D + 8 * c) * 2);
   }
+  auto vchunk = [&](int u, int &d, int &c) __attribute__((always_inline)) {
+    const int pos = 64 * (wave * VDW + u) + lane;
+    d = pos / 8;
+    c = (pos % 8) ^ ((d >> 1) & 7);
+  };
 #pragma unroll
   for (int u = 0; u < VDW; ++u) {
-    const int pos = 64 * (wave * VDW + u) + lane;
-    const int d = pos / 8, c = (pos % 8) ^ ((d >> 1) & 7);
-    vdo_ring[u] = (uint32_t)(((size_t)d * C + 8 * c) * 2);
-    vdo_own[u] = (uint32_t)(((size_t)d * p.n_pad + 8 * c) * 2);
+    int d, c;
+    vchunk(u, d, c);
+    vdo[u] = (uint32_t)((kVBlock * D * (8 * c / kVBlock) + kVBlock * d + 8 * c % kVBlock) * 2);
   }
+  // first ring slot of a partial last block (no such block: never reached)
+  const int vpart = C % kVBlock ? C - C % kVBlock : 0x7fffffff;
   auto dma_k = [&](int t, uint16_t *kb) __attribute__((always_inline)) {
     t = __builtin_amdgcn_readfirstlane(t);  // uniform: the descriptor stays scalar
     const bool own = t >= c01;
@@ -254,10 +265,21 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
     t = __builtin_amdgcn_readfirstlane(t);
     const bool own = t >= c01;
     const __amdgpu_buffer_rsrc_t rv = pick(own, rv_own, rv_ring);
-    const uint32_t sb = (uint32_t)tile_base(t) * 2u;
+    const int base = tile_base(t);
+    if (!own && base + BN > vpart) {
+      // the ring tile reaching the partial last block: per-lane offsets; keys
+      // past C land on later rows (masked) or past the descriptor (read 0)
 #pragma unroll
-    for (int u = 0; u < VDW; ++u)
-      dma16(rv, pick(own, vdo_own[u], vdo_ring[u]) + sb, vb + 512 * (wave * VDW + u));
+      for (int u = 0; u < VDW; ++u) {
+        int d, c;
+        vchunk(u, d, c);
+        dma16(rv, vring_elem(base + 8 * c, d, C, D) * 2u, vb + 512 * (wave * VDW + u));
+      }
+    } else {
+      const uint32_t sb = (uint32_t)base * (uint32_t)(D * 2);
+#pragma unroll
+      for (int u = 0; u < VDW; ++u) dma16(rv, vdo[u] + sb, vb + 512 * (wave * VDW + u));
+    }
   };
   // all of this thread's tile loads have landed in LDS
   auto wait_dma = [&]() __attribute__((always_inline)) {

@@ -16,7 +16,8 @@
 // are loaded in the order that makes a lane's 8 scores 8 consecutive tokens,
 // so the V^T operand of O^T = V^T P^T is one 16-byte load (8 consecutive
 // tokens start at a slot that is a multiple of 8, and C is too, so they never
-// wrap). Combine pass: one block per (query head, KV head, stream) rescales
+// wrap or leave their V block). With C a multiple of 32 a tile is exactly one
+// V block: 64*D contiguous bytes. Combine pass: one block per (query head, KV head, stream) rescales
 // the head's live partials to their common max and normalises.
 #include "frt_launch.hpp"
 
@@ -211,8 +212,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
     query_frag(b, kvh, st.L, qf);
 
     // tile i of the piece: K rows (block kb, A-row rho = c16 -> token
-    // 8*(rho/4) + 4*kb + rho%4 of the tile) and V^T rows (d = 16*db + c16,
-    // tokens 8*g4 .. +8). A piece spans at most C + 62 tokens, so
+    // 8*(rho/4) + 4*kb + rho%4 of the tile) and V rows (d = 16*db + c16,
+    // tokens 8*g4 .. +8, one 16-byte piece of the slot's V block). A piece spans at most C + 62 tokens, so
     // sb0 + 32 i < 2C + 32: at most two wraps.
     auto issue = [&](int i, int buf) __attribute__((always_inline)) {
       int sb = sb0 + kDecTile * i;
@@ -228,10 +229,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
       }
       int vslot = sb + 8 * g4;
       vslot = vslot >= C ? vslot - C : vslot;
+      const uint32_t v0 = vring_elem(vslot, c16, C, D), vw = vring_width(vslot, C);
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
-        vraw[buf][db] =
-            buf_load16(rv, (uint32_t)(((size_t)(16 * db + c16) * C + vslot) * 2));
+        vraw[buf][db] = buf_load16(rv, (v0 + 16 * db * vw) * 2);
     };
 
     f32x4 o[NDB];

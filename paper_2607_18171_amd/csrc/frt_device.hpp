@@ -39,6 +39,23 @@ __device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t b
   return __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 0);
 }
 
+// V ring layout of one (stream, KV head): the C slots are kept in blocks of
+// kVBlock slots, and block k stores its slots row by row of the head
+// dimension, so a block of consecutive keys is one contiguous piece of memory.
+// Element (slot s, row d) sits at kVBlock*D*k + w_k*d + s % kVBlock, where w_k
+// is kVBlock for a full block and C % kVBlock for a partial last block (C is a
+// multiple of 8, so an 8-slot group never leaves its block).
+constexpr int kVBlock = 32;
+// row length w_k of the block holding slot s (0 <= s)
+__device__ __forceinline__ uint32_t vring_width(int s, int C) {
+  const uint32_t k = (uint32_t)s / kVBlock, nfull = (uint32_t)C / kVBlock;
+  return k < nfull ? kVBlock : (uint32_t)C - kVBlock * nfull;
+}
+__device__ __forceinline__ uint32_t vring_elem(int s, int d, int C, int D) {
+  return kVBlock * (uint32_t)D * ((uint32_t)s / kVBlock) + vring_width(s, C) * (uint32_t)d +
+         (uint32_t)s % kVBlock;
+}
+
 // Two packed bf16 values as a vector. Taking the word by value matters:
 // __builtin_bit_cast applied directly to a subscripted vector element has
 // been seen to read element 0 whatever the index.

@@ -24,7 +24,7 @@ struct PrepParams {
   const int64_t *seq_len;
   uint16_t *qr;           // [B][Hkv][n*G][D]    rotated, scaled by qmul
   uint16_t *kr;           // [B][Hkv][n_pad][D]  rotated (stored-key rounding)
-  uint16_t *vt;           // [B][Hkv][D][n_pad]  transposed
+  uint16_t *vt;           // [B][Hkv][n_pad*D]   V ring block layout
   int B, Hq, Hkv, G, D, n, n_pad;
   double qmul;            // softmax scale * log2(e)
 };

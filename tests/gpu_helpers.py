@@ -58,7 +58,7 @@ def build_rings(case: Case, extra_tokens: int = 0):
 
 def ring_bytes_equal(ring: "frt.Ring", oring) -> bool:
     k = from_dev(ring.k)
-    v = np.swapaxes(from_dev(ring.v), 2, 3)
+    v = from_dev(ring.v_tokens())
     sl = ring.seq_len.cpu().numpy()
     return (np.array_equal(k, oring.k) and np.array_equal(v, oring.v)
             and np.array_equal(sl, oring.seq_len))
