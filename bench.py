@@ -2,7 +2,8 @@
 
 A step is the whole hot path for one batch: frt_stream_attn_step (chunk
 preparation + attention) followed by frt_kv_append, or for the decode
-workload frt_decode_attn (split + combine) followed by a one-token append.
+workload frt_decode_step (split + combine, the combine also appending the
+token).
 Inputs are seeded synthetic bf16 tensors already resident in HBM; the ring is
 pre-filled through the library's own append so the measured steps see a
 wrapped ring.
@@ -229,11 +230,11 @@ def main(argv=None):
     torch.cuda.synchronize()
 
     def step():
-        if decode:
-            frt.decode_attn(ring, rope, msk, q, kn, vn, out, ws)
+        if decode:  # attention and the one-token append in one call
+            frt.decode_step(ring, rope, msk, q, kn, vn, out, ws)
         else:
             frt.stream_attn_step(ring, rope, msk, q, kn, vn, out, ws)
-        frt.kv_append(ring, rope, kn, vn)
+            frt.kv_append(ring, rope, kn, vn)
 
     for _ in range(args.warmup):
         step()

@@ -15,10 +15,11 @@
  *
  *   frt_stream_attn_step  READS the ring: out = attention(q, ring keys + own keys)
  *   frt_decode_attn       the same for one token per stream (split-KV + combine)
+ *   frt_decode_step       frt_decode_attn then frt_kv_append, fused (decode loop)
  *   frt_kv_append         WRITES the ring: stores the chunk's RoPE'd K and its V
  *
  * A step is frt_stream_attn_step (or frt_decode_attn) followed by
- * frt_kv_append on the same HIP stream. Attention never sees the chunk through
+ * frt_kv_append on the same HIP stream, or one frt_decode_step. Attention never sees the chunk through
  * the ring: it reads k_new / v_new directly, so a ring whose capacity equals
  * the visible window works even though the append then overwrites the oldest
  * visible chunk.
@@ -213,6 +214,23 @@ size_t frt_decode_workspace_bytes(const frt_ring *ring, int32_t num_q_heads);
  * num_q_heads / num_kv_heads must be <= 16.
  */
 frt_status frt_decode_attn(const frt_ring *ring, const frt_rope *rope,
+                           const frt_mask *mask, const void *q,
+                           const void *k_new, const void *v_new,
+                           int32_t num_q_heads, float softmax_scale,
+                           void *workspace, size_t workspace_bytes, void *out,
+                           float *lse, void *hip_stream);
+
+/*
+ * A whole one-token decode step: exactly frt_decode_attn followed by
+ * frt_kv_append(k_new, v_new, n_new = 1) on the same stream (same outputs,
+ * same ring bytes and seq_len afterwards), in two launches instead of three:
+ * the combine pass also writes each head's slot seq_len mod capacity and
+ * advances seq_len, which is safe because every read of the ring and of
+ * seq_len happens in the split pass before it. Arguments, workspace and
+ * errors as for frt_decode_attn; on an error nothing is launched and the ring
+ * is unchanged.
+ */
+frt_status frt_decode_step(const frt_ring *ring, const frt_rope *rope,
                            const frt_mask *mask, const void *q,
                            const void *k_new, const void *v_new,
                            int32_t num_q_heads, float softmax_scale,

@@ -368,10 +368,12 @@ size_t frt_decode_workspace_bytes(const frt_ring *ring, int32_t num_q_heads) {
          sizeof(float);
 }
 
-frt_status frt_decode_attn(const frt_ring *ring, const frt_rope *rope, const frt_mask *mask,
-                           const void *q, const void *k_new, const void *v_new,
-                           int32_t num_q_heads, float softmax_scale, void *workspace,
-                           size_t workspace_bytes, void *out, float *lse, void *stream) {
+namespace {
+
+frt_status decode_impl(const frt_ring *ring, const frt_rope *rope, const frt_mask *mask,
+                       const void *q, const void *k_new, const void *v_new, int32_t num_q_heads,
+                       float softmax_scale, void *workspace, size_t workspace_bytes, void *out,
+                       float *lse, void *stream, bool append) {
   frt_status s;
   if ((s = check_ring(ring)) != FRT_OK) return s;
   if ((s = check_rope(rope, ring->head_dim)) != FRT_OK) return s;
@@ -396,10 +398,11 @@ frt_status frt_decode_attn(const frt_ring *ring, const frt_rope *rope, const frt
   p.q = static_cast<const uint16_t *>(q);
   p.k_new = static_cast<const uint16_t *>(k_new);
   p.v_new = static_cast<const uint16_t *>(v_new);
-  p.k_ring = static_cast<const uint16_t *>(ring->k_ring);
-  p.v_ring = static_cast<const uint16_t *>(ring->v_ring);
+  p.k_ring = static_cast<uint16_t *>(ring->k_ring);
+  p.v_ring = static_cast<uint16_t *>(ring->v_ring);
   p.seq_len = ring->seq_len;
   p.ws = static_cast<float *>(workspace);
+  p.append = append ? 1 : 0;
   p.out = static_cast<uint16_t *>(out);
   p.lse = lse;
   p.B = ring->num_streams;
@@ -418,6 +421,24 @@ frt_status frt_decode_attn(const frt_ring *ring, const frt_rope *rope, const frt
   if ((s = launch("decode_split", st, [&] { return launch_decode_split(p, rd, st); })) != FRT_OK)
     return s;
   return launch("decode_combine", st, [&] { return launch_decode_combine(p, st); });
+}
+
+}  // namespace
+
+frt_status frt_decode_attn(const frt_ring *ring, const frt_rope *rope, const frt_mask *mask,
+                           const void *q, const void *k_new, const void *v_new,
+                           int32_t num_q_heads, float softmax_scale, void *workspace,
+                           size_t workspace_bytes, void *out, float *lse, void *stream) {
+  return decode_impl(ring, rope, mask, q, k_new, v_new, num_q_heads, softmax_scale, workspace,
+                     workspace_bytes, out, lse, stream, false);
+}
+
+frt_status frt_decode_step(const frt_ring *ring, const frt_rope *rope, const frt_mask *mask,
+                           const void *q, const void *k_new, const void *v_new,
+                           int32_t num_q_heads, float softmax_scale, void *workspace,
+                           size_t workspace_bytes, void *out, float *lse, void *stream) {
+  return decode_impl(ring, rope, mask, q, k_new, v_new, num_q_heads, softmax_scale, workspace,
+                     workspace_bytes, out, lse, stream, true);
 }
 
 frt_status frt_timing_enable(int32_t on) {

@@ -10,7 +10,7 @@
 // step's own token.
 //
 // Split pass tiles stream straight from HBM into MFMA operand registers (no
-// LDS), software-pipelined two tiles deep. All G = Hq/Hkv query heads of the
+// LDS), software-pipelined kDecBufs tiles deep. All G = Hq/Hkv query heads of the
 // KV head are the columns of one 16x16x32 bf16 MFMA, so K and V are read once
 // for the whole group. S^T = K Q^T puts one query per lane column; the K rows
 // are loaded in the order that makes a lane's 8 scores 8 consecutive tokens,
@@ -49,13 +49,13 @@ __device__ __forceinline__ StreamTiles stream_tiles(const DecodeParams &p, int b
   return s;
 }
 
-// Tiles per KV head of streams lane, lane+64, ... summed over the wave:
-// the whole sequence length is Hkv times this.
-__device__ __forceinline__ long long total_tiles(const DecodeParams &p, int lane) {
+// Tiles of every (stream, KV head): the tiles of streams lane, lane+64, ...
+// summed over the wave, times Hkv. n0 is this lane's count for stream lane.
+__device__ __forceinline__ long long total_tiles(const DecodeParams &p, int lane, int n0) {
   long long tot = 0;
   for (int b0 = 0; b0 < p.B; b0 += 64) {
     const int b = b0 + lane;
-    long long n = b < p.B ? stream_tiles(p, b).n : 0;
+    long long n = b0 == 0 ? n0 : (b < p.B ? stream_tiles(p, b).n : 0);
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) n += __shfl_xor(n, off);
     tot += n;
@@ -77,8 +77,41 @@ __device__ __forceinline__ int piece_tiles(const DecodeParams &p, long long T) {
   return (int)(per > kDecChunk ? kDecChunk : per);
 }
 
+// First partial slot and number of pieces of (stream b, KV head kvh), in the
+// order the piece waves take them: streams in order, each stream's KV heads
+// in order, each head's pieces in token order. A wave-wide computation.
+__device__ __forceinline__ void head_pieces(const DecodeParams &p, int lane, int b, int kvh,
+                                            int &K, int &np) {
+  const int n0 = lane < p.B ? stream_tiles(p, lane).n : 0;  // streams 0..63
+  const long long T = total_tiles(p, lane, n0);
+  int n = __shfl(n0, b & 63);
+  if (b >= 64) n = stream_tiles(p, b).n;
+  K = 0;
+  np = 0;
+  if (n > 0) {
+    const int per = piece_tiles(p, T);
+    long long before = 0;  // pieces per KV head of streams before b
+    for (int b0 = 0; b0 < b; b0 += 64) {
+      const int bl = b0 + lane;
+      const int nl = b0 == 0 ? n0 : (bl < p.B ? stream_tiles(p, bl).n : 0);
+      long long c = bl < b ? (nl + per - 1) / per : 0;
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) c += __shfl_xor(c, off);
+      before += c;
+    }
+    np = (n + per - 1) / per;
+    K = (int)(before * p.Hkv) + kvh * np;
+  }
+}
+
+// Own-token partial slot (32-bit words): max[G], sum[G] (= 1), then the
+// head's piece range {K, np}, the query token L as two words, and the key as
+// the ring stores it (D/2 words of bf16 pairs). Its output row is v_new,
+// which the combine pass reads from the input.
+constexpr int kOwnHdr = 4;
+
 template <int D>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void decode_split_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecWavesPerSimd))) void decode_split_kernel(
     DecodeParams p, RopeDev rope) {
   constexpr int NDB = D / 16;  // 16-row d blocks of O^T
   constexpr int NKS = D / 32;  // k-steps of S^T
@@ -112,7 +145,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
   if ((int)blockIdx.x >= own_first) {
     // Partial of the step's own token alone: score = q . k with both rotated
     // and rounded as everywhere else (the key as the append will store it),
-    // sum 1, output v_new.
+    // sum 1, output v_new; plus what the combine pass needs of this head.
     const int h = ((int)blockIdx.x - own_first) * kDecWaves + wave;
     if (h >= H) return;
     const int b = h / p.Hkv, kvh = h % p.Hkv;
@@ -123,11 +156,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
     int co[3];
     rope_coords(rg, L, co);
     float so = 0.f;
+    u32x4 krot[NKS];
 #pragma unroll
     for (int k = 0; k < NKS; ++k) {
       const int d0 = 32 * k + 8 * g4;
       const Rope4 rot = rope_fetch4(rg, co, d0 / 2);
       const u32x4 kr = rotate8_apply(rot, buf_load16(rkn, (uint32_t)(d0 * 2)), 1.0);
+      krot[k] = kr;
       const u32x4 qw = rotate8_apply(rot, buf_load16(rq, (uint32_t)((c16 * D + d0) * 2)), p.qmul);
 #pragma unroll
       for (int w = 0; w < 4; ++w)
@@ -135,22 +170,27 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
     }
     so += __shfl_xor(so, 16);
     so += __shfl_xor(so, 32);
+    int K, np;
+    head_pieces(p, lane, b, kvh, K, np);
     float *part = p.ws + (size_t)(p.nwaves + h) * pfl;
-    if (c16 < G) {
-      // lanes (c16, g4) write output elements d = 32*k + 8*g4 .. +8 of query c16
+    uint32_t *hdr = reinterpret_cast<uint32_t *>(part + 2 * G);
+    if (c16 < G && g4 == 0) {
+      part[c16] = so;
+      part[G + c16] = 1.f;
+    }
+    if (lane == 0) {
+      hdr[0] = (uint32_t)K;
+      hdr[1] = (uint32_t)np;
+      hdr[2] = (uint32_t)(unsigned long long)L;
+      hdr[3] = (uint32_t)((unsigned long long)L >> 32);
+    }
+    if (c16 == 0) {
+      // the rotated key (every c16 holds it): d chunk 32*k + 8*g4
 #pragma unroll
       for (int k = 0; k < NKS; ++k) {
         const int d0 = 32 * k + 8 * g4;
-        const u32x4 v = *reinterpret_cast<const u32x4 *>(p.v_new + (size_t)h * D + d0);
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          part[2 * G + c16 * D + d0 + 2 * w] = bf16_bits_to_f32(v[w] & 0xFFFFu);
-          part[2 * G + c16 * D + d0 + 2 * w + 1] = bf16_bits_to_f32(v[w] >> 16);
-        }
-      }
-      if (g4 == 0) {
-        part[c16] = so;
-        part[G + c16] = 1.f;
+        for (int w = 0; w < 4; ++w) hdr[kOwnHdr + d0 / 2 + w] = krot[k][w];
       }
     }
     return;
@@ -159,7 +199,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
   // ---- piece wave: pieces are consecutive runs of at most `per` tiles of one
   // (stream, KV head); wave wv takes piece wv ----
   const int wv = (int)blockIdx.x * kDecWaves + wave;
-  const long long T = total_tiles(p, lane);
+  const int n0 = lane < p.B ? stream_tiles(p, lane).n : 0;  // streams 0..63, kept
+  const long long T = total_tiles(p, lane, n0);
   if (T == 0) return;
   const int per = piece_tiles(p, T);
   // the stream holding piece wv: Kb = index of its first piece
@@ -168,7 +209,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
   bool found = false;
   for (int b0 = 0; b0 < p.B; b0 += 64) {
     const int bl = b0 + lane;
-    const long long np = bl < p.B ? (long long)((stream_tiles(p, bl).n + per - 1) / per) * p.Hkv : 0;
+    const int nl = b0 == 0 ? n0 : (bl < p.B ? stream_tiles(p, bl).n : 0);
+    const long long np = (long long)((nl + per - 1) / per) * p.Hkv;
     long long incl = np;  // inclusive scan over the wave
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
@@ -193,8 +235,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
     const int kvh = (int)((wv - Kb) / pc);
     const int j0 = (int)((wv - Kb) % pc) * per;
     const int cnt = min(st.n - j0, per);
-    u32x4 kraw[2][2][NKS];
-    u32x4 vraw[2][NDB];
+    u32x4 kraw[kDecBufs][2][NKS];
+    u32x4 vraw[kDecBufs][NDB];
     bf16x8 qf[NKS];
     const size_t head = (size_t)b * p.Hkv + kvh;
     const __amdgpu_buffer_rsrc_t rk = make_rsrc(p.k_ring + head * (size_t)C * D,
@@ -240,13 +282,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
     for (int db = 0; db < NDB; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
     float m = kNegInf, lsum = 0.f;
 
-    // the piece's tiles, unrolled so that the two register buffers stay
+    // the piece's tiles, unrolled so that the register buffers stay
     // statically indexed; tiles past cnt are skipped (uniform branches)
-    issue(0, 0);
-    if (cnt > 1) issue(1, 1);
+#pragma unroll
+    for (int j = 0; j < kDecBufs; ++j)
+      if (j < cnt) issue(j, j);
 #pragma unroll
     for (int i = 0; i < kDecChunk; ++i) {
-      const int buf = i & 1;
+      const int buf = i % kDecBufs;
       if (i < cnt) {
         f32x4 sacc[2];
 #pragma unroll
@@ -291,7 +334,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
               __builtin_bit_cast(bf16x8, vraw[buf][db]), pf, o[db], 0, 0, 0);
         }
       }
-      if (i + 2 < cnt) issue(i + 2, buf);
+      if (i + kDecBufs < cnt) issue(i + kDecBufs, buf);
     }
 
     // partial of this piece in slot (wave + head): lane column c16 = query,
@@ -315,106 +358,84 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
 }
 
 // Combine pass: one block of D threads per (query head, KV head, stream);
-// thread d owns output column d. The head's partials are its pieces (slots
-// wave + head for the waves whose ranges cover its tiles) and its own-token
-// partial. The live ones (positive sum; the own token's always is) of a
-// chunk of D candidates are listed in LDS with their weights 2^(m_s - M); the
-// output column then sums over the list with independent, coalesced loads.
+// thread d owns output column d. The head's partials are its pieces (their
+// slot range is recorded in the own-token slot by the split pass) and its
+// own-token partial. Partials
+// are merged online in groups of kCombineGroup: the (max, sum, column) loads
+// of a group are independent, so after the stream lengths are known the pass
+// waits on memory once per group.
+constexpr int kCombineGroup = 16;
+
 template <int D>
 __global__ __launch_bounds__(D) void decode_combine_kernel(DecodeParams p) {
-  constexpr int NW = D / 64;  // waves per block
-  __shared__ int lidx[D];
-  __shared__ float lwt[D], lsm[D];
-  __shared__ float red[NW];
-  __shared__ int cnt[NW];
-
   const int q = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int t = threadIdx.x;
   const int G = p.G;
   const int head = b * p.Hkv + kvh;
   const int hq = kvh * G + q;
   const size_t pstride = decode_split_floats(G, D);
 
-  // the head's pieces: slots K .. K+np-1, K = pieces of the heads before it
-  const long long T = total_tiles(p, lane);
-  const int n = stream_tiles(p, b).n;
-  int K = 0, np = 0;
-  if (n > 0) {
-    const int per = piece_tiles(p, T);
-    long long before = 0;  // pieces per KV head of streams before b
-    for (int b0 = 0; b0 < b; b0 += 64) {
-      const int bl = b0 + lane;
-      long long c = bl < b ? (stream_tiles(p, bl).n + per - 1) / per : 0;
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) c += __shfl_xor(c, off);
-      before += c;
-    }
-    np = (n + per - 1) / per;
-    K = (int)(before * p.Hkv) + kvh * np;
-  }
+  // the head's pieces (slots K .. K+np-1) and query token, as the split
+  // pass recorded them in the own-token slot; seq_len is not read here, so
+  // that an appending combine may advance it
+  const float *own = p.ws + (size_t)(p.nwaves + head) * pstride;
+  const uint32_t *hdr = reinterpret_cast<const uint32_t *>(own + 2 * G);
+  const int K = (int)hdr[0], np = (int)hdr[1];
+  const long long L = (long long)((unsigned long long)hdr[2] | ((unsigned long long)hdr[3] << 32));
   const int ncand = np + 1;  // pieces, then the own token
-  auto slot_of = [&](int c) { return c < np ? K + c : p.nwaves + head; };
 
-  // common max over every live candidate
-  float mx = kNegInf;
-  for (int c = t; c < ncand; c += D) {
-    const float *pp = p.ws + (size_t)slot_of(c) * pstride;
-    if (pp[G + q] > 0.f) mx = fmaxf(mx, pp[q]);
-  }
+  float M = kNegInf, acc = 0.f, lt = 0.f;
+  for (int c0 = 0; c0 < ncand; c0 += kCombineGroup) {
+    float mv[kCombineGroup], lv[kCombineGroup], ov[kCombineGroup];
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
-  if (lane == 0) red[wave] = mx;
-  __syncthreads();
-  float M = kNegInf;
+    for (int j = 0; j < kCombineGroup; ++j) {
+      const int c = c0 + j;
+      mv[j] = kNegInf;
+      lv[j] = 0.f;
+      ov[j] = 0.f;
+      if (c < np) {
+        const float *pp = p.ws + (size_t)(K + c) * pstride;
+        mv[j] = pp[q];
+        lv[j] = pp[G + q];
+        ov[j] = pp[2 * G + q * D + t];
+      } else if (c == np) {
+        mv[j] = own[q];
+        lv[j] = own[G + q];
+        ov[j] = bf16_bits_to_f32(p.v_new[(size_t)head * D + t]);
+      }
+    }
+    // live partials have a positive sum (the own token's always has)
+    float Mg = M;
 #pragma unroll
-  for (int w = 0; w < NW; ++w) M = fmaxf(M, red[w]);
-
-  float lt = 0.f, acc = 0.f;
-  const float *ocol = p.ws + 2 * G + (size_t)q * D + t;
-  for (int base = 0; base < ncand; base += D) {
-    const int c = base + t;
-    float ls = 0.f, ms = 0.f;
-    int s = 0;
-    if (c < ncand) {
-      s = slot_of(c);
-      ls = p.ws[(size_t)s * pstride + G + q];
-      ms = p.ws[(size_t)s * pstride + q];
-    }
-    const bool live = ls > 0.f;
-    const uint64_t bal = __ballot(live);
-    const int pos = __builtin_popcountll(bal & ((1ull << lane) - 1ull));
-    if (lane == 0) cnt[wave] = __builtin_popcountll(bal);
-    __syncthreads();
-    int off = 0, nl = 0;
+    for (int j = 0; j < kCombineGroup; ++j) Mg = lv[j] > 0.f ? fmaxf(Mg, mv[j]) : Mg;
+    if (Mg != kNegInf) {
+      const float a = __builtin_amdgcn_exp2f(M - Mg);  // M = -inf gives 0
+      acc *= a;
+      lt *= a;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      off += w < wave ? cnt[w] : 0;
-      nl += cnt[w];
+      for (int j = 0; j < kCombineGroup; ++j) {
+        const float w = lv[j] > 0.f ? __builtin_amdgcn_exp2f(mv[j] - Mg) : 0.f;
+        acc += ov[j] * w;
+        lt += lv[j] * w;
+      }
+      M = Mg;
     }
-    if (live) {
-      const float f = __builtin_amdgcn_exp2f(ms - M);
-      lidx[off + pos] = s;
-      lwt[off + pos] = f;
-      lsm[off + pos] = ls * f;
-    }
-    __syncthreads();
-    int i = 0;
-    for (; i + 4 <= nl; i += 4) {
-      const float o0 = ocol[(size_t)lidx[i] * pstride], o1 = ocol[(size_t)lidx[i + 1] * pstride];
-      const float o2 = ocol[(size_t)lidx[i + 2] * pstride],
-                  o3 = ocol[(size_t)lidx[i + 3] * pstride];
-      acc += o0 * lwt[i] + o1 * lwt[i + 1] + o2 * lwt[i + 2] + o3 * lwt[i + 3];
-      lt += lsm[i] + lsm[i + 1] + lsm[i + 2] + lsm[i + 3];
-    }
-    for (; i < nl; ++i) {
-      acc += ocol[(size_t)lidx[i] * pstride] * lwt[i];
-      lt += lsm[i];
-    }
-    __syncthreads();
   }
   p.out[((size_t)b * p.Hq + hq) * D + t] = (uint16_t)f32_to_bf16_rne(acc / lt);
   if (t == 0 && p.lse != nullptr)
     p.lse[(size_t)b * p.Hq + hq] = (M + __builtin_amdgcn_logf(lt)) * 0.6931471805599453f;
+
+  // the append: the split pass has finished every read of the ring and of
+  // seq_len, and no combine block reads either
+  if (p.append && q == 0) {
+    const int slot = (int)(L % p.C);
+    if (t < D / 2)
+      reinterpret_cast<uint32_t *>(p.k_ring + ((size_t)head * p.C + slot) * D)[t] =
+          hdr[kOwnHdr + t];
+    p.v_ring[(size_t)head * D * p.C + vring_elem(slot, t, p.C, D)] =
+        p.v_new[(size_t)head * D + t];
+    if (kvh == 0 && t == 0) p.seq_len[b] = L + 1;
+  }
 }
 
 }  // namespace

@@ -44,14 +44,15 @@ struct DecodeParams {
   const uint16_t *q;       // [B][1][Hq][D]
   const uint16_t *k_new;   // [B][1][Hkv][D]
   const uint16_t *v_new;   // [B][1][Hkv][D]
-  const uint16_t *k_ring, *v_ring;
-  const int64_t *seq_len;
+  uint16_t *k_ring, *v_ring;  // written only by the combine pass, and only with append
+  int64_t *seq_len;
   float *ws;               // partials: nwaves + B * Hkv
   uint16_t *out;           // [B][1][Hq][D]
   float *lse;              // [B][Hq][1] or null
   int B, Hq, Hkv, G, D, C;
   int nwaves;              // piece waves of the split pass (multiple of 4)
   int mask_kind, mask_block, mask_window;
+  int append;              // combine pass also appends the token to the ring
   double qmul;
 };
 
@@ -63,8 +64,10 @@ constexpr int kChunkBN = 64;        // keys per attention tile
 #endif
 constexpr int kChunkWaves = FRT_ATTN_WAVES;  // waves per attention block
 constexpr int kChunkRows = 32 * kChunkWaves;  // query rows per block (32 per wave)
-constexpr int kDecResident = 2048;  // decode split waves resident at once (2 per SIMD)
-constexpr int kDecChunk = 12;       // most 32-token tiles of one decode piece
+constexpr int kDecWavesPerSimd = 2;  // decode split occupancy (register bound)
+constexpr int kDecBufs = 2;          // decode split tiles in flight per wave
+constexpr int kDecResident = 256 * 4 * kDecWavesPerSimd;  // split waves resident at once
+constexpr int kDecChunk = 12;        // most 32-token tiles of one decode piece
 
 // Floats of one decode partial: max[G], sum[G], out[G][D].
 // Piece waves of a decode call: enough for every split of the tiles

@@ -30,7 +30,7 @@ def declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = frt.load_library()
     names = declared_symbols()
-    assert len(names) == 13
+    assert len(names) == 14
     for name in names:
         assert hasattr(lib, name), name
     assert sorted(B.EXPORTS) == names
@@ -115,12 +115,13 @@ def test_decode_rejects_bad_arguments():
     assert waves == (2048 + 1 + 3) // 4 * 4
     assert wsb == (waves + 1) * 8 * (2 + 128) * 4
 
-    def dec(hq=8, ws=FAKE, n=wsb):
-        return lib.frt_decode_attn(ctypes.byref(r), ctypes.byref(o), ctypes.byref(m), FAKE, FAKE,
-                                   FAKE, hq, 0.0, ws, n, FAKE, None, None)
-    assert dec(hq=17) == 3
-    assert dec(ws=0) == 6
-    assert dec(n=wsb - 4) == 6
+    for fn in (lib.frt_decode_attn, lib.frt_decode_step):
+        def dec(hq=8, ws=FAKE, n=wsb):
+            return fn(ctypes.byref(r), ctypes.byref(o), ctypes.byref(m), FAKE, FAKE, FAKE, hq, 0.0,
+                      ws, n, FAKE, None, None)
+        assert dec(hq=17) == 3
+        assert dec(ws=0) == 6
+        assert dec(n=wsb - 4) == 6
 
 
 def test_workspace_sizes():

@@ -1,13 +1,15 @@
-"""frt_decode_attn (split-KV + combine) on the GPU against the fp64 oracle."""
+"""frt_decode_attn (split-KV + combine) and frt_decode_step on the GPU against the fp64
+oracle."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
 import paper_2607_18171_amd as frt
-from workloads import WORKLOADS, RopeSpec, MaskSpec, ROPE_1D, MASK_CAUSAL, MASK_BLOCK_CAUSAL, make_case, shrink
+from workloads import (WORKLOADS, RopeSpec, MaskSpec, ROPE_1D, MASK_CAUSAL, MASK_BLOCK_CAUSAL,
+                       make_case, shrink, draw_bf16)
 from gpu_helpers import (to_dev, bf16_dev_to_f64, build_rings, gpu_mask, visible_vmax,
-                         check_close)
+                         check_close, ring_bytes_equal)
 
 pytestmark = pytest.mark.gpu
 
@@ -59,3 +61,37 @@ def test_decode_equals_stream_step_with_one_token():
     frt.stream_attn_step(ring, rope, gpu_mask(wl), q, k, v, b, ws)
     torch.cuda.synchronize()
     check_close(bf16_dev_to_f64(a), bf16_dev_to_f64(b), visible_vmax(oring, case), "decode vs step")
+
+
+@pytest.mark.parametrize("name", ["split_edges", "mha", "g16_d64", "wrapped_window"])
+def test_decode_step_equals_attn_then_append(name):
+    """frt_decode_step over consecutive steps: the same outputs and lse as
+    frt_decode_attn + frt_kv_append, bit for bit, and the same ring bytes and
+    lengths, which also match the oracle's ring exactly."""
+    wl, lengths = CASES[name]
+    case = make_case(wl, 3, lengths=np.array(lengths))
+    steps = 4
+    ring, oring, rope = build_rings(case, extra_tokens=steps + 1)
+    twin = frt.Ring(wl.B, wl.Hkv, wl.d, wl.C, k=ring.k.clone(), v=ring.v.clone(),
+                    seq_len=ring.seq_len.clone())
+    ws = torch.empty(frt.decode_workspace_bytes(ring, wl.Hq), dtype=torch.uint8, device="cuda")
+    ws2 = torch.empty_like(ws)
+    rng = np.random.default_rng(11)
+    for s in range(steps):
+        kn = draw_bf16(rng, case.k_new.shape)  # a fresh token each step
+        vn = draw_bf16(rng, case.v_new.shape)
+        q, k, v = to_dev(case.q), to_dev(kn), to_dev(vn)
+        out_a, out_b = torch.empty_like(q), torch.empty_like(q)
+        lse_a = torch.empty((wl.B, wl.Hq, 1), dtype=torch.float32, device="cuda")
+        lse_b = torch.empty_like(lse_a)
+        frt.decode_attn(twin, rope, gpu_mask(wl), q, k, v, out_a, ws2, lse=lse_a)
+        frt.kv_append(twin, rope, k, v)
+        frt.decode_step(ring, rope, gpu_mask(wl), q, k, v, out_b, ws, lse=lse_b)
+        torch.cuda.synchronize()
+        assert torch.equal(out_a.view(torch.int16), out_b.view(torch.int16)), (name, s)
+        assert torch.equal(lse_a, lse_b), (name, s)
+        assert torch.equal(ring.k.view(torch.int16), twin.k.view(torch.int16)), (name, s)
+        assert torch.equal(ring.v.view(torch.int16), twin.v.view(torch.int16)), (name, s)
+        assert torch.equal(ring.seq_len, twin.seq_len), (name, s)
+        oring = oracle.kv_append(oring, kn, vn, wl.rope)
+    assert ring_bytes_equal(ring, oring)
