@@ -419,9 +419,6 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
       __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);  // VALU
     }
     if (!tile_fast(t + 1)) {
-      // a real branch: without a side effect here the compiler turns the
-      // block into selects, and every tile would pay for the mask
-      asm volatile("; edge tile");
       mask_tile(t + 1, snext);
       mt = row_max(snext);
     }
