@@ -1,9 +1,9 @@
 """Benchmark one streaming step of chunk-streamed attention on one MI355X.
 
-A step is the whole hot path for one batch: frt_stream_attn_step (chunk
-preparation + attention) followed by frt_kv_append, or for the decode
-workload frt_decode_step (split + combine, the combine also appending the
-token).
+A step is the whole hot path for one batch: frt_stream_step (chunk
+preparation, attention, and the append of the prepared chunk), or for the
+decode workload frt_decode_step (split + combine, the combine also appending
+the token).
 Inputs are seeded synthetic bf16 tensors already resident in HBM; the ring is
 pre-filled through the library's own append so the measured steps see a
 wrapped ring.
@@ -233,8 +233,7 @@ def main(argv=None):
         if decode:  # attention and the one-token append in one call
             frt.decode_step(ring, rope, msk, q, kn, vn, out, ws)
         else:
-            frt.stream_attn_step(ring, rope, msk, q, kn, vn, out, ws)
-            frt.kv_append(ring, rope, kn, vn)
+            frt.stream_step(ring, rope, msk, q, kn, vn, out, ws)
 
     for _ in range(args.warmup):
         step()
@@ -272,8 +271,8 @@ def main(argv=None):
     frt.timing_enable(False)
 
     kernels = {}
-    for name in ("chunk_prep", "chunk_attn", "decode_split", "decode_combine", "rope_append",
-                 "seq_advance"):
+    for name in ("chunk_prep", "chunk_attn", "chunk_append", "decode_split", "decode_combine",
+                 "rope_append", "seq_advance"):
         c, ms = frt.timing_query(name)
         if c:
             kernels[name] = {"launches": c, "avg_us": 1000.0 * ms / c}

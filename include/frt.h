@@ -14,12 +14,13 @@
  * cached keys plus its own. This library implements that step:
  *
  *   frt_stream_attn_step  READS the ring: out = attention(q, ring keys + own keys)
+ *   frt_stream_step       frt_stream_attn_step then frt_kv_append, fused
  *   frt_decode_attn       the same for one token per stream (split-KV + combine)
  *   frt_decode_step       frt_decode_attn then frt_kv_append, fused (decode loop)
  *   frt_kv_append         WRITES the ring: stores the chunk's RoPE'd K and its V
  *
  * A step is frt_stream_attn_step (or frt_decode_attn) followed by
- * frt_kv_append on the same HIP stream, or one frt_decode_step. Attention never sees the chunk through
+ * frt_kv_append on the same HIP stream, or one frt_stream_step / frt_decode_step. Attention never sees the chunk through
  * the ring: it reads k_new / v_new directly, so a ring whose capacity equals
  * the visible window works even though the append then overwrites the oldest
  * visible chunk.
@@ -163,8 +164,9 @@ frt_status frt_kv_append(const frt_ring *ring, const frt_rope *rope,
                          void *hip_stream);
 
 /*
- * Workspace bytes frt_stream_attn_step needs: the chunk's rotated, scaled
- * queries and own keys and its transposed own values (bf16), rounded up.
+ * Workspace bytes frt_stream_attn_step and frt_stream_step need: the chunk's
+ * rotated, scaled queries and own keys and its own values in the ring's block
+ * layout (bf16), and each stream's seq_len at the step's start, rounded up.
  */
 size_t frt_stream_attn_workspace_bytes(const frt_ring *ring, int32_t n_new,
                                        int32_t num_q_heads);
@@ -193,6 +195,25 @@ frt_status frt_stream_attn_step(const frt_ring *ring, const frt_rope *rope,
                                 float softmax_scale, void *workspace,
                                 size_t workspace_bytes, void *out, float *lse,
                                 void *hip_stream);
+
+/*
+ * A whole streaming step: exactly frt_stream_attn_step followed by
+ * frt_kv_append(k_new, v_new, n_new) on the same stream (same outputs, same
+ * ring bytes and seq_len afterwards). The append copies the keys the step
+ * has already rotated and rounded as the ring stores them from the workspace,
+ * with the values from v_new, and advances seq_len in the same launch: three
+ * launches instead of four, and no second rotation. The append
+ * runs after the attention launch has finished reading the ring (the oldest
+ * visible chunk may occupy the slots it overwrites). Arguments, workspace
+ * and errors as for frt_stream_attn_step; n_new <= capacity.
+ */
+frt_status frt_stream_step(const frt_ring *ring, const frt_rope *rope,
+                           const frt_mask *mask, const void *q,
+                           const void *k_new, const void *v_new,
+                           int32_t n_new, int32_t num_q_heads,
+                           float softmax_scale, void *workspace,
+                           size_t workspace_bytes, void *out, float *lse,
+                           void *hip_stream);
 
 /* Largest number of KV pieces a decode call splits the ring into (one
  * partial each): every (stream, KV head) is cut into pieces of consecutive
@@ -247,7 +268,7 @@ const char *frt_last_error(void);
  * Built-in kernel timing. When enabled, every kernel the library launches
  * is bracketed by HIP events on its stream. frt_timing_query waits for the
  * recorded events of `kernel` (one of "rope_append", "seq_advance",
- * "chunk_prep", "chunk_attn", "decode_split", "decode_combine") and returns
+ * "chunk_prep", "chunk_attn", "chunk_append", "decode_split", "decode_combine") and returns
  * their count and summed milliseconds; frt_timing_reset drops all records.
  */
 frt_status frt_timing_enable(int32_t on);

@@ -26,7 +26,8 @@ MASK_BLOCK_CAUSAL, MASK_CAUSAL = 1, 2
 # every symbol include/frt.h declares
 EXPORTS = (
     "frt_rope_table_bytes", "frt_rope_table_fill", "frt_kv_append",
-    "frt_stream_attn_workspace_bytes", "frt_stream_attn_step", "frt_decode_max_splits",
+    "frt_stream_attn_workspace_bytes", "frt_stream_attn_step", "frt_stream_step",
+    "frt_decode_max_splits",
     "frt_decode_workspace_bytes", "frt_decode_attn", "frt_decode_step", "frt_status_str",
     "frt_last_error",
     "frt_timing_enable", "frt_timing_query", "frt_timing_reset",
@@ -82,6 +83,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "frt_stream_attn_workspace_bytes": (SZ, [RP, I32, I32]),
         "frt_stream_attn_step": (I32, [RP, OP, MP, P, P, P, I32, I32, ctypes.c_float, P, SZ, P,
                                        P, P]),
+        "frt_stream_step": (I32, [RP, OP, MP, P, P, P, I32, I32, ctypes.c_float, P, SZ, P,
+                                  P, P]),
         "frt_decode_max_splits": (I32, [RP]),
         "frt_decode_workspace_bytes": (SZ, [RP, I32]),
         "frt_decode_attn": (I32, [RP, OP, MP, P, P, P, I32, ctypes.c_float, P, SZ, P, P, P]),
@@ -239,6 +242,17 @@ def stream_attn_step(ring: Ring, rope: Rope, msk: CMask, q, k_new, v_new, out, w
     n, hq = q.shape[1], q.shape[2]
     cr, co = ring.c(), rope.c()
     _check(load_library().frt_stream_attn_step(
+        ctypes.byref(cr), ctypes.byref(co), ctypes.byref(msk), _ptr(q), _ptr(k_new), _ptr(v_new),
+        n, hq, softmax_scale, _ptr(workspace), workspace.numel() * workspace.element_size(),
+        _ptr(out), _ptr(lse), _stream(stream)))
+
+
+def stream_step(ring: Ring, rope: Rope, msk: CMask, q, k_new, v_new, out, workspace,
+                lse=None, softmax_scale: float = 0.0, stream=None) -> None:
+    """frt_stream_step: stream_attn_step then kv_append, fused."""
+    n, hq = q.shape[1], q.shape[2]
+    cr, co = ring.c(), rope.c()
+    _check(load_library().frt_stream_step(
         ctypes.byref(cr), ctypes.byref(co), ctypes.byref(msk), _ptr(q), _ptr(k_new), _ptr(v_new),
         n, hq, softmax_scale, _ptr(workspace), workspace.numel() * workspace.element_size(),
         _ptr(out), _ptr(lse), _stream(stream)))

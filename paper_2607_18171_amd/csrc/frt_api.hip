@@ -171,7 +171,7 @@ double q_multiplier(float softmax_scale, int d) {
 }
 
 struct StepLayout {
-  size_t q_off, k_off, v_off, bytes;
+  size_t q_off, k_off, v_off, l_off, bytes;
   int n_pad;
 };
 
@@ -182,7 +182,8 @@ StepLayout step_layout(const frt_ring *r, int n, int hq) {
   L.q_off = 0;
   L.k_off = round_up((size_t)r->num_streams * n * hq * d * 2, 256);
   L.v_off = L.k_off + round_up((size_t)r->num_streams * r->num_kv_heads * L.n_pad * d * 2, 256);
-  L.bytes = L.v_off + round_up((size_t)r->num_streams * r->num_kv_heads * L.n_pad * d * 2, 256);
+  L.l_off = L.v_off + round_up((size_t)r->num_streams * r->num_kv_heads * L.n_pad * d * 2, 256);
+  L.bytes = L.l_off + round_up((size_t)r->num_streams * 8, 256);
   return L;
 }
 
@@ -279,10 +280,12 @@ size_t frt_stream_attn_workspace_bytes(const frt_ring *ring, int32_t n_new, int3
   return step_layout(ring, n_new, num_q_heads).bytes;
 }
 
-frt_status frt_stream_attn_step(const frt_ring *ring, const frt_rope *rope, const frt_mask *mask,
-                                const void *q, const void *k_new, const void *v_new, int32_t n_new,
-                                int32_t num_q_heads, float softmax_scale, void *workspace,
-                                size_t workspace_bytes, void *out, float *lse, void *stream) {
+namespace {
+
+frt_status stream_impl(const frt_ring *ring, const frt_rope *rope, const frt_mask *mask,
+                       const void *q, const void *k_new, const void *v_new, int32_t n_new,
+                       int32_t num_q_heads, float softmax_scale, void *workspace,
+                       size_t workspace_bytes, void *out, float *lse, void *stream, bool append) {
   frt_status s;
   if ((s = check_ring(ring)) != FRT_OK) return s;
   if ((s = check_rope(rope, ring->head_dim)) != FRT_OK) return s;
@@ -317,6 +320,7 @@ frt_status frt_stream_attn_step(const frt_ring *ring, const frt_rope *rope, cons
   pp.qr = reinterpret_cast<uint16_t *>(ws + lay.q_off);
   pp.kr = reinterpret_cast<uint16_t *>(ws + lay.k_off);
   pp.vt = reinterpret_cast<uint16_t *>(ws + lay.v_off);
+  pp.lrec = reinterpret_cast<int64_t *>(ws + lay.l_off);
   pp.B = ring->num_streams;
   pp.Hq = num_q_heads;
   pp.Hkv = ring->num_kv_heads;
@@ -351,7 +355,44 @@ frt_status frt_stream_attn_step(const frt_ring *ring, const frt_rope *rope, cons
   hipStream_t st = static_cast<hipStream_t>(stream);
   if ((s = launch("chunk_prep", st, [&] { return launch_chunk_prep(pp, rd, st); })) != FRT_OK)
     return s;
-  return launch("chunk_attn", st, [&] { return launch_chunk_attn(ap, ring->head_dim, st); });
+  if ((s = launch("chunk_attn", st, [&] { return launch_chunk_attn(ap, ring->head_dim, st); })) !=
+          FRT_OK ||
+      !append)
+    return s;
+  ChunkAppendParams cp;
+  cp.kr = pp.kr;
+  cp.v_new = pp.v_new;
+  cp.lrec = pp.lrec;
+  cp.k_ring = static_cast<uint16_t *>(ring->k_ring);
+  cp.v_ring = static_cast<uint16_t *>(ring->v_ring);
+  cp.seq_len = ring->seq_len;
+  cp.B = pp.B;
+  cp.Hkv = pp.Hkv;
+  cp.D = pp.D;
+  cp.C = ring->capacity;
+  cp.n = n_new;
+  cp.n_pad = lay.n_pad;
+  return launch("chunk_append", st, [&] { return launch_chunk_append(cp, st); });
+}
+
+}  // namespace
+
+frt_status frt_stream_attn_step(const frt_ring *ring, const frt_rope *rope, const frt_mask *mask,
+                                const void *q, const void *k_new, const void *v_new, int32_t n_new,
+                                int32_t num_q_heads, float softmax_scale, void *workspace,
+                                size_t workspace_bytes, void *out, float *lse, void *stream) {
+  return stream_impl(ring, rope, mask, q, k_new, v_new, n_new, num_q_heads, softmax_scale,
+                     workspace, workspace_bytes, out, lse, stream, false);
+}
+
+frt_status frt_stream_step(const frt_ring *ring, const frt_rope *rope, const frt_mask *mask,
+                           const void *q, const void *k_new, const void *v_new, int32_t n_new,
+                           int32_t num_q_heads, float softmax_scale, void *workspace,
+                           size_t workspace_bytes, void *out, float *lse, void *stream) {
+  if (ring && n_new > ring->capacity)
+    return fail(FRT_ERR_CAPACITY, "n_new=%d > capacity=%d", n_new, ring->capacity);
+  return stream_impl(ring, rope, mask, q, k_new, v_new, n_new, num_q_heads, softmax_scale,
+                     workspace, workspace_bytes, out, lse, stream, true);
 }
 
 int32_t frt_decode_max_splits(const frt_ring *ring) {

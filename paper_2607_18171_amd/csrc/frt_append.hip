@@ -103,6 +103,7 @@ __global__ __launch_bounds__(256) void chunk_prep_kernel(PrepParams p, RopeDev r
   const long long L = p.seq_len[b];
   const int t0 = tb * kAppendTokens;
   const size_t head = (size_t)b * p.Hkv + kvh;
+  if (tb == 0 && kvh == 0 && threadIdx.x == 0) p.lrec[b] = L;
 
   // own keys (stored-key rounding) and values into LDS; zero padding rows
   for (int idx = threadIdx.x; idx < kAppendTokens * CH; idx += 256) {
@@ -154,7 +155,58 @@ __global__ __launch_bounds__(256) void chunk_prep_kernel(PrepParams p, RopeDev r
   }
 }
 
+// The append half of a fused step: the chunk's keys are already rotated and
+// rounded exactly as frt_kv_append stores them, so they are copied; values
+// take the transposing path of rope_append_kernel. seq_len is read by no
+// block of this kernel (L comes from the record the preparation pass left),
+// so one block per stream can advance it.
+template <int D>
+__global__ __launch_bounds__(256) void chunk_append_kernel(ChunkAppendParams p) {
+  constexpr int CH = D / 8;  // 16-byte chunks per row
+  constexpr int VS = D + 2;  // LDS row stride (elements), odd dword count
+  __shared__ uint16_t vs[kAppendTokens * VS];
+  const int tb = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const long long L = p.lrec[b];
+  const int t0 = tb * kAppendTokens;
+  const int ntok = min(kAppendTokens, p.n - t0);
+  const size_t head = (size_t)b * p.Hkv + kvh;
+  const uint16_t *krh = p.kr + head * (size_t)p.n_pad * D;
+  for (int idx = threadIdx.x; idx < kAppendTokens * CH; idx += 256) {
+    const int r = idx / CH, c = idx % CH;
+    if (r >= ntok) continue;
+    const int i = t0 + r;
+    const int slot = (int)((L + i) % p.C);
+    *reinterpret_cast<u32x4 *>(p.k_ring + (head * p.C + slot) * D + c * 8) =
+        *reinterpret_cast<const u32x4 *>(krh + (size_t)i * D + c * 8);
+    const u32x4 v =
+        *reinterpret_cast<const u32x4 *>(p.v_new + (((size_t)b * p.n + i) * p.Hkv + kvh) * D + c * 8);
+    uint32_t *dst = reinterpret_cast<uint32_t *>(vs + r * VS + c * 8);
+    dst[0] = v[0];
+    dst[1] = v[1];
+    dst[2] = v[2];
+    dst[3] = v[3];
+  }
+  __syncthreads();
+  const int r = threadIdx.x & 63;
+  if (r < ntok) {
+    const int slot = (int)((L + t0 + r) % p.C);
+    uint16_t *vdst = p.v_ring + head * (size_t)D * p.C + vring_elem(slot, 0, p.C, D);
+    const uint32_t w = vring_width(slot, p.C);
+    for (int dd = threadIdx.x >> 6; dd < D; dd += 4) vdst[dd * w] = vs[r * VS + dd];
+  }
+  if (tb == 0 && kvh == 0 && threadIdx.x == 0) p.seq_len[b] = L + p.n;
+}
+
 }  // namespace
+
+hipError_t launch_chunk_append(const ChunkAppendParams &p, hipStream_t s) {
+  dim3 grid((p.n + kAppendTokens - 1) / kAppendTokens, p.Hkv, p.B);
+  if (p.D == 128)
+    hipLaunchKernelGGL(chunk_append_kernel<128>, grid, dim3(256), 0, s, p);
+  else
+    hipLaunchKernelGGL(chunk_append_kernel<64>, grid, dim3(256), 0, s, p);
+  return hipGetLastError();
+}
 
 hipError_t launch_rope_append(const AppendParams &p, const RopeDev &r, hipStream_t s) {
   dim3 grid((p.n + kAppendTokens - 1) / kAppendTokens, p.Hkv, p.B);

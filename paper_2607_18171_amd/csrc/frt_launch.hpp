@@ -12,9 +12,21 @@ struct AppendParams {
   const uint16_t *k_new;  // [B][n][Hkv][D]
   const uint16_t *v_new;  // [B][n][Hkv][D]
   uint16_t *k_ring;       // [B][Hkv][C][D]
-  uint16_t *v_ring;       // [B][Hkv][D][C]
+  uint16_t *v_ring;       // [B][Hkv][C*D]   32-slot blocks
   int64_t *seq_len;       // [B]
   int B, Hkv, D, C, n;
+};
+
+// Append of a prepared chunk: the rotated keys of the step workspace and the
+// values v_new go to slots (L + i) mod C, L as the preparation pass recorded
+// it; seq_len becomes L + n.
+struct ChunkAppendParams {
+  const uint16_t *kr;     // [B][Hkv][n_pad][D]
+  const uint16_t *v_new;  // [B][n][Hkv][D]
+  const int64_t *lrec;    // [B]  seq_len at the step's start
+  uint16_t *k_ring, *v_ring;
+  int64_t *seq_len;
+  int B, Hkv, D, C, n, n_pad;
 };
 
 struct PrepParams {
@@ -25,6 +37,7 @@ struct PrepParams {
   uint16_t *qr;           // [B][Hkv][n*G][D]    rotated, scaled by qmul
   uint16_t *kr;           // [B][Hkv][n_pad][D]  rotated (stored-key rounding)
   uint16_t *vt;           // [B][Hkv][n_pad*D]   V ring block layout
+  int64_t *lrec;          // [B]  seq_len at the step's start, recorded
   int B, Hq, Hkv, G, D, n, n_pad;
   double qmul;            // softmax scale * log2(e)
 };
@@ -88,6 +101,7 @@ hipError_t launch_rope_append_small(const AppendParams &p, const RopeDev &r, hip
 hipError_t launch_seq_advance(int64_t *seq_len, int B, int n, hipStream_t s);
 hipError_t launch_chunk_prep(const PrepParams &p, const RopeDev &r, hipStream_t s);
 hipError_t launch_chunk_attn(const AttnParams &p, int D, hipStream_t s);
+hipError_t launch_chunk_append(const ChunkAppendParams &p, hipStream_t s);
 hipError_t launch_decode_split(const DecodeParams &p, const RopeDev &r, hipStream_t s);
 hipError_t launch_decode_combine(const DecodeParams &p, hipStream_t s);
 

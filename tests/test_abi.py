@@ -30,7 +30,7 @@ def declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = frt.load_library()
     names = declared_symbols()
-    assert len(names) == 14
+    assert len(names) == 15
     for name in names:
         assert hasattr(lib, name), name
     assert sorted(B.EXPORTS) == names
@@ -129,7 +129,9 @@ def test_workspace_sizes():
     r = ring(B_=1, H=12, d=128, C=18720)
     got = lib.frt_stream_attn_workspace_bytes(ctypes.byref(r), 4680, 12)
     n_pad = 4736
-    expect = 4680 * 12 * 128 * 2 + 2 * (12 * n_pad * 128 * 2)
+    # rotated queries, own keys, own values (each a multiple of 256 bytes here),
+    # then one int64 per stream, rounded up to 256 bytes
+    expect = 4680 * 12 * 128 * 2 + 2 * (12 * n_pad * 128 * 2) + 256
     assert got == expect
 
 

@@ -12,9 +12,9 @@ import torch
 import oracle
 import paper_2607_18171_amd as frt
 from workloads import (WORKLOADS, RopeSpec, MaskSpec, ROPE_1D, ROPE_3D, ROPE_NONE,
-                       MASK_BLOCK_CAUSAL, MASK_CAUSAL, make_case, shrink)
+                       MASK_BLOCK_CAUSAL, MASK_CAUSAL, make_case, shrink, draw_bf16)
 from gpu_helpers import (to_dev, from_dev, bf16_dev_to_f64, build_rings, gpu_mask,
-                         visible_vmax, check_close)
+                         visible_vmax, check_close, ring_bytes_equal)
 
 pytestmark = pytest.mark.gpu
 
@@ -158,3 +158,38 @@ def test_deterministic_and_checkpoint_restore():
     assert torch.equal(x.view(torch.int16), y.view(torch.int16))
     assert torch.equal(ring.k.view(torch.int16), saved.k.view(torch.int16))
     assert torch.equal(ring.v.view(torch.int16), saved.v.view(torch.int16))
+
+
+@pytest.mark.parametrize("name", ["video_small", "video_vpart", "gqa_swa", "gqa_d64"])
+def test_stream_step_equals_attn_then_append(name):
+    """frt_stream_step over consecutive steps: the same outputs and lse as
+    frt_stream_attn_step + frt_kv_append, bit for bit, the same ring bytes and
+    lengths, and a ring equal to the oracle's."""
+    wl = SMALL[name]
+    case = make_case(wl, 4)
+    steps = 3
+    ring, oring, rope = build_rings(case, extra_tokens=steps * wl.n)
+    twin = frt.Ring(wl.B, wl.Hkv, wl.d, wl.C, k=ring.k.clone(), v=ring.v.clone(),
+                    seq_len=ring.seq_len.clone())
+    nbytes = frt.stream_attn_workspace_bytes(ring, wl.n, wl.Hq)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    ws2 = torch.empty_like(ws)
+    rng = np.random.default_rng(12)
+    for s in range(steps):
+        kn = draw_bf16(rng, case.k_new.shape)  # a fresh chunk each step
+        vn = draw_bf16(rng, case.v_new.shape)
+        q, k, v = to_dev(case.q), to_dev(kn), to_dev(vn)
+        out_a, out_b = torch.empty_like(q), torch.empty_like(q)
+        lse_a = torch.empty((wl.B, wl.Hq, wl.n), dtype=torch.float32, device="cuda")
+        lse_b = torch.empty_like(lse_a)
+        frt.stream_attn_step(twin, rope, gpu_mask(wl), q, k, v, out_a, ws2, lse=lse_a)
+        frt.kv_append(twin, rope, k, v)
+        frt.stream_step(ring, rope, gpu_mask(wl), q, k, v, out_b, ws, lse=lse_b)
+        torch.cuda.synchronize()
+        assert torch.equal(out_a.view(torch.int16), out_b.view(torch.int16)), (name, s)
+        assert torch.equal(lse_a, lse_b), (name, s)
+        assert torch.equal(ring.k.view(torch.int16), twin.k.view(torch.int16)), (name, s)
+        assert torch.equal(ring.v.view(torch.int16), twin.v.view(torch.int16)), (name, s)
+        assert torch.equal(ring.seq_len, twin.seq_len), (name, s)
+        oring = oracle.kv_append(oring, kn, vn, wl.rope)
+    assert ring_bytes_equal(ring, oring)
