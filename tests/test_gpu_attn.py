@@ -91,7 +91,7 @@ def _sample_rows(wl, rng, extra):
     return np.array(sorted(r for r in rows if 0 <= r < wl.n))
 
 
-@pytest.mark.parametrize("name", ["video_1p3b", "video_14b", "prefill_swa"])
+@pytest.mark.parametrize("name", ["video_1p3b", "video_14b", "prefill_swa", "video_1p3b_pp4"])
 def test_full_size_sampled_rows(name):
     wl = WORKLOADS[name]
     case = make_case(wl, 0)

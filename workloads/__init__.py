@@ -72,6 +72,7 @@ class Workload:
     len_lo: int = -1       # per-stream prior lengths ~ U{len_lo..len_hi}
     len_hi: int = -1
     qk_scale: float = 1.0  # Q and K drawn N(0,1)*qk_scale
+    stagger: int = 0       # stream b holds prior_steps + stagger*(B-1-b) chunks
     description: str = ""
 
     @property
@@ -80,7 +81,7 @@ class Workload:
 
     @property
     def per_stream_lengths(self) -> bool:
-        return self.len_lo >= 0
+        return self.len_lo >= 0 or self.stagger > 0
 
 
 WORKLOADS = {
@@ -100,6 +101,12 @@ WORKLOADS = {
         mask=MaskSpec(MASK_BLOCK_CAUSAL, 4680, 6), prior_steps=9,
         qk_scale=float(np.sqrt(3.0)),
         description="B1 H40 d128, 4680-token chunk vs 28080 cached + own, wrapped ring"),
+    "video_1p3b_pp4": Workload(
+        "video_1p3b_pp4", B=4, Hq=12, Hkv=12, d=128, n=4680, C=18720,
+        rope=RopeSpec(ROPE_3D, (44, 42, 42), (30, 52)),
+        mask=MaskSpec(MASK_BLOCK_CAUSAL, 4680, 4), prior_steps=6, stagger=1,
+        description="4 denoising-step caches of the 1.3B-like step as 4 streams, one "
+                    "chunk apart (the stages of a step pipeline), one launch"),
     "decode": Workload(
         "decode", B=32, Hq=32, Hkv=4, d=128, n=1, C=8448,
         rope=RopeSpec(ROPE_1D, (128, 0, 0)),
@@ -157,7 +164,11 @@ def make_case(wl, seed: int = 0, lengths: Optional[np.ndarray] = None) -> Case:
     rng = np.random.default_rng(seed)
     s = wl.qk_scale
     if wl.per_stream_lengths:
-        drawn = rng.integers(wl.len_lo, wl.len_hi, wl.B, endpoint=True).astype(np.int64)
+        if wl.stagger > 0:
+            drawn = np.array([(wl.prior_steps + wl.stagger * (wl.B - 1 - b)) * wl.n
+                              for b in range(wl.B)], dtype=np.int64)
+        else:
+            drawn = rng.integers(wl.len_lo, wl.len_hi, wl.B, endpoint=True).astype(np.int64)
         if lengths is not None:
             drawn = np.asarray(lengths, dtype=np.int64)
         fills = []
