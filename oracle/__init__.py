@@ -35,7 +35,8 @@ append happens after); scale 1/sqrt(d); GQA query head h uses KV head
 h // (Hq/Hkv).
 
 Modules: rope (tables, rotation, rounding), ring (append, slot map),
-attention (masked attention, decode), brute (pure-Python loop twins).
+attention (masked attention, decode), brute (pure-Python loop twins), fp8
+(the e4m3fn codec and the FP8 KV-cache / FP8 QK^T-PV variant of the step).
 """
 from .rope import (rope_cos_sin, rope_positions, rotate_f64, round_f64_to_bf16,
                    bf16_to_f64, stored_k)

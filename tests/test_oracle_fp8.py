@@ -1,0 +1,215 @@
+"""Pins of the FP8 (e4m3fn) oracle, CPU only: the codec against torch's
+float8_e4m3fn, ties and clamping, the power-of-two query row scale by brute
+force, closed forms of the FP8 attention (uniform scores, one dominant key),
+and a pure-Python loop twin on tiny cases."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import fp8
+from workloads import (RopeSpec, MaskSpec, ROPE_1D, ROPE_NONE, MASK_CAUSAL,
+                       MASK_BLOCK_CAUSAL)
+from _helpers import rand_bits
+
+
+def test_decode_matches_torch_for_every_code():
+    codes = np.arange(256, dtype=np.uint8)
+    ref = torch.from_numpy(codes).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    got = fp8.e4m3_decode(codes)
+    assert np.array_equal(np.isnan(got), np.isnan(ref))
+    ok = ~np.isnan(ref)
+    assert np.array_equal(got[ok], ref[ok])
+    assert math.copysign(1.0, got[0x80]) == -1.0  # -0 keeps its sign
+    assert np.isnan(got[0x7f]) and np.isnan(got[0xff]) and got[0x7e] == 448.0
+
+
+def test_encode_matches_torch_in_range():
+    rng = np.random.default_rng(0)
+    x = np.concatenate([rng.standard_normal(20000) * s for s in (1e-3, 0.05, 1.0, 30.0, 200.0)])
+    pos = fp8.e4m3_decode(np.arange(0x7f, dtype=np.uint8))
+    mids = (pos[1:] + pos[:-1]) / 2  # every tie
+    x = np.concatenate([x, pos, -pos, mids, -mids, np.nextafter(mids, 0.0),
+                        np.nextafter(mids, 1e9), [0.0, -0.0]])
+    x = x[np.abs(x) <= 448].astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(fp8.e4m3_encode(x.astype(np.float64)), ref)
+
+
+def test_encode_clamps_out_of_range():
+    got = fp8.e4m3_encode(np.array([464.0, 470.0, 1e9, -1e9, -470.0]))
+    assert got.tolist() == [0x7e, 0x7e, 0x7e, 0xfe, 0xfe]
+
+
+def test_ties_go_to_the_even_code():
+    # halfway 1.0 (0x38) / 1.125 (0x39) -> 0x38; 1.125 / 1.25 (0x3a) -> 0x3a
+    assert fp8.e4m3_encode(np.array([1.0625, 1.1875])).tolist() == [0x38, 0x3a]
+
+
+def test_pow2_row_exponent_brute_force():
+    rng = np.random.default_rng(1)
+    a = rng.standard_normal((400, 8)) * np.exp2(rng.integers(-30, 30, (400, 1)))
+    a[0] = 0.0
+    a[1, 0] = 448.0
+    a[2, 0] = np.nextafter(np.float32(448.0), np.float32(1e9))
+    a[3, 0] = 224.0
+    a = a.astype(np.float32)
+    e = fp8.pow2_row_exponent(a)
+    for row, ei in zip(a, e):
+        mx = float(np.abs(row.astype(np.float64)).max())
+        if mx == 0.0:
+            assert ei == 0
+            continue
+        k = -300
+        while mx > 448.0 * 2.0 ** k:
+            k += 1
+        assert ei == k
+    assert e[1] == 0 and e[2] == 1 and e[3] == -1
+
+
+def _filled_ring(rng, B, Hkv, C, d, steps, rope, ks, vs):
+    ring = fp8.RingFP8(B, Hkv, C, d)
+    for s in steps:
+        fp8.kv_append_fp8(ring, rand_bits(rng, (B, s, Hkv, d)), rand_bits(rng, (B, s, Hkv, d)),
+                          rope, ks, vs)
+    return ring
+
+
+def test_append_quantises_as_defined():
+    rng = np.random.default_rng(2)
+    rope = RopeSpec(ROPE_1D, (16, 0, 0))
+    ks = np.array([[0.5, 0.01]], np.float32)
+    vs = np.array([[2.0, 0.25]], np.float32)
+    ring = _filled_ring(rng, 1, 2, 8, 16, [5, 6], rope, ks, vs)
+    assert ring.seq_len.tolist() == [11]
+    # token 10 sits in slot 2; a saturating scale clamps to +-448
+    k = rand_bits(rng, (1, 1, 2, 16))
+    v = rand_bits(rng, (1, 1, 2, 16))
+    fp8.kv_append_fp8(ring, k, v, rope, ks, vs)
+    rot = oracle.rotate_f64(k[0, :, 1, :], np.array([11]), rope).astype(np.float32)
+    want = fp8.e4m3_encode((rot / np.float32(0.01)).astype(np.float64))
+    assert np.array_equal(ring.k[0, 1, 3], want[0])
+    assert np.all(np.abs(fp8.e4m3_decode(ring.k[0, 1, 3])) <= 448)
+    vv = oracle.bf16_to_f64(v[0, 0, 0]).astype(np.float32)
+    assert np.array_equal(ring.v[0, 0, 3], fp8.e4m3_encode((vv / np.float32(2.0)).astype(np.float64)))
+
+
+def test_uniform_scores_give_the_mean_of_stored_values():
+    rng = np.random.default_rng(3)
+    rope = RopeSpec(ROPE_1D, (16, 0, 0))
+    mask = MaskSpec(MASK_CAUSAL, 0, 0)
+    ks = np.ones((2, 1), np.float32)
+    vs = np.array([[0.5], [3.0]], np.float32)
+    ring = _filled_ring(rng, 2, 1, 16, 16, [7], rope, ks, vs)
+    n = 3
+    q = np.zeros((2, n, 2, 16), np.uint16)  # zero queries: every score is 0
+    k = rand_bits(rng, (2, n, 1, 16))
+    v = rand_bits(rng, (2, n, 1, 16))
+    out, lse = fp8.stream_attn_fp8(ring, q, k, v, rope, mask, ks, vs)
+    for b in range(2):
+        V = np.concatenate([fp8.e4m3_decode(ring.k[b, 0][:0]).reshape(0, 16),
+                            fp8.e4m3_decode(ring.v[b, 0][:7]),
+                            fp8.e4m3_decode(fp8.stored_v8(v[b, :, 0, :], vs[b, 0]))])
+        for i in range(n):
+            want = vs[b, 0] * V[:7 + i + 1].mean(axis=0)
+            assert np.allclose(out[b, i, 0], want, rtol=0, atol=1e-12)
+            assert np.allclose(out[b, i, 1], want, rtol=0, atol=1e-12)
+            assert abs(lse[b, 0, i] - math.log(7 + i + 1)) < 1e-12
+
+
+def test_one_dominant_key_gives_its_value():
+    rope = RopeSpec(ROPE_NONE)
+    mask = MaskSpec(MASK_BLOCK_CAUSAL, 2, 0)
+    d = 16
+    ks = np.ones((1, 1), np.float32)
+    vs = np.array([[0.125]], np.float32)
+    ring = fp8.RingFP8(1, 1, 8, d)
+    rng = np.random.default_rng(4)
+    kz = np.zeros((1, 4, 1, d), np.uint16)
+    kz[0, 2, 0, :] = 0x4200  # bf16 32.0 in every dimension: token 2 dominates
+    fp8.kv_append_fp8(ring, kz, rand_bits(rng, (1, 4, 1, d)), rope, ks, vs)
+    q = np.full((1, 2, 1, d), 0x3f80, np.uint16)  # bf16 1.0
+    out, _ = fp8.stream_attn_fp8(ring, q, np.zeros((1, 2, 1, d), np.uint16),
+                                 rand_bits(rng, (1, 2, 1, d)), rope, mask, ks, vs)
+    want = 0.125 * fp8.e4m3_decode(ring.v[0, 0, 2])
+    assert np.array_equal(out[0, 0, 0], want) and np.array_equal(out[0, 1, 0], want)
+
+
+def _twin(ring, q, k_new, v_new, rope, mask, ks, vs):
+    """Loop form of the FP8 step with its own nearest-code search."""
+    values = [fp8.e4m3_value(c) for c in range(256)]
+
+    def enc(x):
+        a = min(abs(x), 448.0)
+        best = None
+        for c in range(0x7f):
+            dist = abs(a - values[c])
+            if best is None or dist < best[0] or (dist == best[0] and c % 2 == 0):
+                best = (dist, c)
+        return best[1] | (0x80 if math.copysign(1.0, x) < 0 else 0)
+
+    B, n, Hq, d = q.shape
+    Hkv = k_new.shape[2]
+    G = Hq // Hkv
+    mul = (1.0 / math.sqrt(d)) * math.log2(math.e)
+    out = np.zeros((B, n, Hq, d))
+    for b in range(B):
+        L = int(ring.seq_len[b])
+        C = ring.C
+        for i in range(n):
+            p_tok = L + i
+            for hq in range(Hq):
+                h = hq // G
+                sk, sv = float(ks[b, h]), float(vs[b, h])
+                keys = []
+                for tok in range(max(0, L - C), L):
+                    keys.append((tok, [values[c] for c in ring.k[b, h, tok % C]],
+                                 [values[c] for c in ring.v[b, h, tok % C]]))
+                for j in range(n):
+                    tok = L + j
+                    kr = oracle.rotate_f64(k_new[b, j:j + 1, h, :], np.array([tok]), rope)[0]
+                    kc = [enc(float(np.float32(np.float32(x) / np.float32(sk)))) for x in kr]
+                    vc = [enc(float(np.float32(np.float32(x) / np.float32(sv))))
+                          for x in oracle.bf16_to_f64(v_new[b, j, h, :])]
+                    keys.append((tok, [values[c] for c in kc], [values[c] for c in vc]))
+                a = [float(np.float32(x * mul)) for x in
+                     oracle.rotate_f64(q[b, i:i + 1, hq, :], np.array([p_tok]), rope)[0]]
+                mx = max(abs(x) for x in a)
+                e = 0
+                if mx > 0:
+                    e = -300
+                    while mx > 448.0 * 2.0 ** e:
+                        e += 1
+                qv = [values[enc(x * 2.0 ** -e)] for x in a]
+                scored = []
+                for tok, kv, vv in keys:
+                    if oracle.visible(mask, p_tok, tok):
+                        s = 2.0 ** e * sk * sum(qv[t] * kv[t] for t in range(d))
+                        scored.append((s, vv))
+                m = math.ceil(max(s for s, _ in scored))
+                w = [values[enc(2.0 ** (s - m))] for s, _ in scored]
+                tot = sum(w)
+                for t in range(d):
+                    out[b, i, hq, t] = sv * sum(wk * vv[t] for wk, (_, vv) in zip(w, scored)) / tot
+    return out
+
+
+@pytest.mark.parametrize("rope,mask,B,Hq,Hkv,C,steps,n", [
+    (RopeSpec(ROPE_1D, (16, 0, 0)), MaskSpec(MASK_CAUSAL, 0, 0), 1, 2, 1, 8, [5], 3),
+    (RopeSpec(ROPE_1D, (16, 0, 0)), MaskSpec(MASK_BLOCK_CAUSAL, 3, 1), 2, 2, 2, 6, [3, 3], 3),
+    (RopeSpec(ROPE_NONE), MaskSpec(MASK_CAUSAL, 0, 4), 1, 4, 2, 8, [6], 2),
+])
+def test_vectorised_matches_loop_twin(rope, mask, B, Hq, Hkv, C, steps, n):
+    rng = np.random.default_rng(5)
+    d = 16
+    ks = rng.uniform(0.002, 0.02, (B, Hkv)).astype(np.float32)
+    vs = rng.uniform(0.002, 0.02, (B, Hkv)).astype(np.float32)
+    ring = _filled_ring(rng, B, Hkv, C, d, steps, rope, ks, vs)
+    q = rand_bits(rng, (B, n, Hq, d), 2.0)
+    k = rand_bits(rng, (B, n, Hkv, d))
+    v = rand_bits(rng, (B, n, Hkv, d))
+    out, _ = fp8.stream_attn_fp8(ring, q, k, v, rope, mask, ks, vs)
+    ref = _twin(ring, q, k, v, rope, mask, ks, vs)
+    assert np.allclose(out, ref, rtol=0, atol=1e-12)
