@@ -258,6 +258,52 @@ frt_status frt_decode_step(const frt_ring *ring, const frt_rope *rope,
                            void *workspace, size_t workspace_bytes, void *out,
                            float *lse, void *hip_stream);
 
+/*
+ * FP8 variant (the FP8 KV cache with FP8 Q.K^T and P.V). The ring holds
+ * OCP e4m3fn codes (1 sign, 4 exponent bits with bias 7, 3 mantissa bits;
+ * largest finite 448, 0x7f / 0xff NaN), same layouts as above with one-byte
+ * elements. A code c of stream b, KV head h stands for value(c) * scale:
+ *   k_scale, v_scale: fp32 [num_streams][num_kv_heads], device memory, > 0.
+ * Coding: x / scale in fp32, clamped to +-448, rounded to nearest (ties to
+ * the even code); keys are rotated as for the bf16 ring and rounded to fp32
+ * before the division. Not a paper passage: the format and rounding follow
+ * the OCP 8-bit floating point specification.
+ */
+typedef struct {
+  const float *k_scale;
+  const float *v_scale;
+} frt_fp8_scales;
+
+/* frt_kv_append for an FP8 ring: the same slots and seq_len update, the
+ * values stored as codes. head_dim 64 or 128. */
+frt_status frt_kv_append_fp8(const frt_ring *ring, const frt_fp8_scales *scales,
+                             const frt_rope *rope, const void *k_new,
+                             const void *v_new, int32_t n_new, void *hip_stream);
+
+/* Workspace bytes frt_stream_attn_step_fp8 needs: query codes and their row
+ * scales, the chunk's own key and value codes. */
+size_t frt_stream_attn_fp8_workspace_bytes(const frt_ring *ring, int32_t n_new,
+                                           int32_t num_q_heads);
+
+/*
+ * frt_stream_attn_step over an FP8 ring (head_dim 128). Queries are rotated
+ * and scaled to base-2 score units in double, rounded to fp32 and coded with
+ * a power-of-two scale per query row (the smallest 2^e with max|a| <= 448 *
+ * 2^e); the chunk's own keys and values are coded as the append will store
+ * them. Both contractions are FP8 MFMAs with fp32 accumulation; the
+ * attention weights are coded too, p = code(2^(s - m + 7)) with m the
+ * smallest integer >= the row's largest score (s in base-2 units), and
+ * out = v_scale * sum(p v) / sum(p) with both sums over the coded weights. Same tensors, checks and errors as
+ * frt_stream_attn_step, plus FRT_ERR_UNSUPPORTED for head_dim != 128.
+ */
+frt_status frt_stream_attn_step_fp8(const frt_ring *ring, const frt_fp8_scales *scales,
+                                    const frt_rope *rope, const frt_mask *mask,
+                                    const void *q, const void *k_new,
+                                    const void *v_new, int32_t n_new,
+                                    int32_t num_q_heads, float softmax_scale,
+                                    void *workspace, size_t workspace_bytes,
+                                    void *out, float *lse, void *hip_stream);
+
 /* Static description of a status code. */
 const char *frt_status_str(frt_status status);
 

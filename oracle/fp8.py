@@ -19,8 +19,12 @@ listed with the others in the design notes:
     e the smallest integer with max|a| <= 448 * 2^e;
   * scores s = 2^e * s_k * (q8 . k8) in base-2 units; with m the smallest
     integer >= the row's largest visible score, the weights are
-    p = q8(2^(s - m)) and out = s_v * sum(p * v8) / sum(p), so the sum and
-    the product use the same quantised weights.
+    p = q8(2^(s - m + 7)) and out = s_v * sum(p * v8) / sum(p), so the sum
+    and the product use the same quantised weights. The factor 2^7 puts the
+    largest weight in [64, 128] and the first subnormal code 2^-13 below it:
+    a row whose softmax mass is spread (3x unit logits over tens of
+    thousands of keys leave the top key a few percent of it) keeps that mass
+    in normal codes instead of flushing it to zero.
 
 Pins: tests/test_oracle_fp8.py (every code against the format's definition,
 rounding ties, the closed forms of uniform and one-hot attention, and the
@@ -37,6 +41,7 @@ from .ring import slots_of_tokens
 from .attention import visible
 
 E4M3_MAX = 448.0
+P_SHIFT = 7  # weights are coded at 2^P_SHIFT times their ratio to 2^m
 
 
 def e4m3_value(code: int) -> float:
@@ -185,8 +190,8 @@ def stream_attn_fp8(ring: RingFP8, q, k_new, v_new, rope, mask, k_scale, v_scale
                 vis = visible(mask, ptok[:, None], ktok[None, :])
                 s = np.where(vis, s, -np.inf)
                 m = np.ceil(s.max(axis=1, keepdims=True))
-                p = e4m3_decode(e4m3_encode(np.exp2(s - m)))
+                p = e4m3_decode(e4m3_encode(np.exp2(s - m + P_SHIFT)))
                 l = p.sum(axis=1, keepdims=True)
                 out[b, sel, hq, :] = sv * (p @ V) / l
-                lse[b, hq, sel] = ((m + np.log2(l)) * math.log(2.0))[:, 0]
+                lse[b, hq, sel] = ((m - P_SHIFT + np.log2(l)) * math.log(2.0))[:, 0]
     return out, lse

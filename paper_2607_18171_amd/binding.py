@@ -28,7 +28,8 @@ EXPORTS = (
     "frt_rope_table_bytes", "frt_rope_table_fill", "frt_kv_append",
     "frt_stream_attn_workspace_bytes", "frt_stream_attn_step", "frt_stream_step",
     "frt_decode_max_splits",
-    "frt_decode_workspace_bytes", "frt_decode_attn", "frt_decode_step", "frt_status_str",
+    "frt_decode_workspace_bytes", "frt_decode_attn", "frt_decode_step", "frt_kv_append_fp8",
+    "frt_stream_attn_fp8_workspace_bytes", "frt_stream_attn_step_fp8", "frt_status_str",
     "frt_last_error",
     "frt_timing_enable", "frt_timing_query", "frt_timing_reset",
 )
@@ -57,6 +58,10 @@ class CMask(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("block", ctypes.c_int32), ("window", ctypes.c_int32)]
 
 
+class CFp8Scales(ctypes.Structure):
+    _fields_ = [("k_scale", ctypes.c_void_p), ("v_scale", ctypes.c_void_p)]
+
+
 _lib = None
 
 
@@ -76,6 +81,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     I32 = ctypes.c_int32
     SZ = ctypes.c_size_t
     RP, OP, MP = ctypes.POINTER(CRing), ctypes.POINTER(CRope), ctypes.POINTER(CMask)
+    SP = ctypes.POINTER(CFp8Scales)
     sig = {
         "frt_rope_table_bytes": (SZ, [OP]),
         "frt_rope_table_fill": (I32, [OP, P, SZ]),
@@ -89,6 +95,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "frt_decode_workspace_bytes": (SZ, [RP, I32]),
         "frt_decode_attn": (I32, [RP, OP, MP, P, P, P, I32, ctypes.c_float, P, SZ, P, P, P]),
         "frt_decode_step": (I32, [RP, OP, MP, P, P, P, I32, ctypes.c_float, P, SZ, P, P, P]),
+        "frt_kv_append_fp8": (I32, [RP, SP, OP, P, P, I32, P]),
+        "frt_stream_attn_fp8_workspace_bytes": (SZ, [RP, I32, I32]),
+        "frt_stream_attn_step_fp8": (I32, [RP, SP, OP, MP, P, P, P, I32, I32, ctypes.c_float, P,
+                                           SZ, P, P, P]),
         "frt_status_str": (ctypes.c_char_p, [I32]),
         "frt_last_error": (ctypes.c_char_p, []),
         "frt_timing_enable": (I32, [I32]),
@@ -288,6 +298,59 @@ def decode_step(ring: Ring, rope: Rope, msk: CMask, q, k_new, v_new, out, worksp
         ctypes.byref(cr), ctypes.byref(co), ctypes.byref(msk), _ptr(q), _ptr(k_new), _ptr(v_new),
         hq, softmax_scale, _ptr(workspace), workspace.numel() * workspace.element_size(),
         _ptr(out), _ptr(lse), _stream(stream)))
+
+
+# ------------------------------------------------------------------ FP8 --
+class RingFp8(Ring):
+    """An FP8 (e4m3fn) ring: k uint8 [B][Hkv][C][d], v uint8 [B][Hkv][C*d] in
+    32-slot blocks, and fp32 [B][Hkv] dequantisation scales k_scale / v_scale."""
+
+    def __init__(self, num_streams: int, num_kv_heads: int, head_dim: int, capacity: int,
+                 k_scale, v_scale, device="cuda"):
+        import torch
+        k = torch.zeros((num_streams, num_kv_heads, capacity, head_dim), dtype=torch.uint8,
+                        device=device)
+        v = torch.zeros((num_streams, num_kv_heads, capacity * head_dim), dtype=torch.uint8,
+                        device=device)
+        super().__init__(num_streams, num_kv_heads, head_dim, capacity, device=device, k=k, v=v)
+        self.k_scale = k_scale.to(device=device, dtype=torch.float32).contiguous()
+        self.v_scale = v_scale.to(device=device, dtype=torch.float32).contiguous()
+
+    def scales(self) -> CFp8Scales:
+        return CFp8Scales(_ptr(self.k_scale), _ptr(self.v_scale))
+
+    def view_stream(self, b: int) -> "RingFp8":
+        """A one-stream view sharing memory (and scales) with stream b."""
+        view = RingFp8.__new__(RingFp8)
+        Ring.__init__(view, 1, self.Hkv, self.d, self.C, k=self.k[b:b + 1], v=self.v[b:b + 1],
+                      seq_len=self.seq_len[b:b + 1])
+        view.k_scale, view.v_scale = self.k_scale[b:b + 1], self.v_scale[b:b + 1]
+        return view
+
+
+def kv_append_fp8(ring: RingFp8, rope: Rope, k_new, v_new, stream=None) -> None:
+    """frt_kv_append_fp8: k_new/v_new bf16 [B][n][Hkv][d]."""
+    cr, co, cs = ring.c(), rope.c(), ring.scales()
+    _check(load_library().frt_kv_append_fp8(ctypes.byref(cr), ctypes.byref(cs), ctypes.byref(co),
+                                            _ptr(k_new), _ptr(v_new), k_new.shape[1],
+                                            _stream(stream)))
+
+
+def stream_attn_fp8_workspace_bytes(ring: Ring, n_new: int, num_q_heads: int) -> int:
+    cr = ring.c()
+    return int(load_library().frt_stream_attn_fp8_workspace_bytes(ctypes.byref(cr), n_new,
+                                                                  num_q_heads))
+
+
+def stream_attn_step_fp8(ring: RingFp8, rope: Rope, msk: CMask, q, k_new, v_new, out, workspace,
+                         lse=None, softmax_scale: float = 0.0, stream=None) -> None:
+    """frt_stream_attn_step_fp8: q/out bf16 [B][n][Hq][d]."""
+    n, hq = q.shape[1], q.shape[2]
+    cr, co, cs = ring.c(), rope.c(), ring.scales()
+    _check(load_library().frt_stream_attn_step_fp8(
+        ctypes.byref(cr), ctypes.byref(cs), ctypes.byref(co), ctypes.byref(msk), _ptr(q),
+        _ptr(k_new), _ptr(v_new), n, hq, softmax_scale, _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _ptr(out), _ptr(lse), _stream(stream)))
 
 
 def timing_enable(on: bool = True) -> None:

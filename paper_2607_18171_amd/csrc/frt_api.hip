@@ -395,6 +395,160 @@ frt_status frt_stream_step(const frt_ring *ring, const frt_rope *rope, const frt
                      workspace, workspace_bytes, out, lse, stream, true);
 }
 
+// ---------------------------------------------------------------- FP8 --
+namespace {
+
+struct Fp8Layout {
+  size_t q_off, s_off, k_off, v_off, bytes;
+  int n_pad;
+};
+
+Fp8Layout fp8_layout(const frt_ring *r, int n, int hq) {
+  Fp8Layout L;
+  const size_t d = (size_t)r->head_dim;
+  const size_t rows = (size_t)r->num_streams * n * hq;  // query rows of all heads
+  L.n_pad = (int)round_up((size_t)n, kChunkBN);
+  L.q_off = 0;
+  L.s_off = round_up(rows * d, 256);
+  L.k_off = L.s_off + round_up(rows * 4, 256);
+  L.v_off = L.k_off + round_up((size_t)r->num_streams * r->num_kv_heads * L.n_pad * d, 256);
+  L.bytes = L.v_off + round_up((size_t)r->num_streams * r->num_kv_heads * L.n_pad * d, 256);
+  return L;
+}
+
+frt_status check_scales(const frt_fp8_scales *sc) {
+  if (!sc || !sc->k_scale || !sc->v_scale) return fail(FRT_ERR_NULL, "FP8 scales are NULL");
+  if (!aligned(sc->k_scale, 4) || !aligned(sc->v_scale, 4))
+    return fail(FRT_ERR_ALIGN, "FP8 scales must be 4-byte aligned");
+  return FRT_OK;
+}
+
+}  // namespace
+
+frt_status frt_kv_append_fp8(const frt_ring *ring, const frt_fp8_scales *scales,
+                             const frt_rope *rope, const void *k_new, const void *v_new,
+                             int32_t n_new, void *stream) {
+  frt_status s;
+  if ((s = check_ring(ring)) != FRT_OK) return s;
+  if ((s = check_scales(scales)) != FRT_OK) return s;
+  if ((s = check_rope(rope, ring->head_dim)) != FRT_OK) return s;
+  if (n_new < 0) return fail(FRT_ERR_SHAPE, "n_new=%d < 0", n_new);
+  if (n_new > ring->capacity)
+    return fail(FRT_ERR_CAPACITY, "n_new=%d > capacity=%d", n_new, ring->capacity);
+  if (n_new == 0) return FRT_OK;
+  if ((s = check_io(k_new, "k_new")) != FRT_OK) return s;
+  if ((s = check_io(v_new, "v_new")) != FRT_OK) return s;
+  AppendFp8Params p;
+  p.k_new = static_cast<const uint16_t *>(k_new);
+  p.v_new = static_cast<const uint16_t *>(v_new);
+  p.k_ring = static_cast<uint8_t *>(ring->k_ring);
+  p.v_ring = static_cast<uint8_t *>(ring->v_ring);
+  p.seq_len = ring->seq_len;
+  p.sc.k = scales->k_scale;
+  p.sc.v = scales->v_scale;
+  p.B = ring->num_streams;
+  p.Hkv = ring->num_kv_heads;
+  p.D = ring->head_dim;
+  p.C = ring->capacity;
+  p.n = n_new;
+  const RopeDev rd = rope_dev(rope);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if ((s = launch("rope_append", st, [&] { return launch_rope_append_fp8(p, rd, st); })) != FRT_OK)
+    return s;
+  return launch("seq_advance", st, [&] { return launch_seq_advance(ring->seq_len, p.B, n_new, st); });
+}
+
+size_t frt_stream_attn_fp8_workspace_bytes(const frt_ring *ring, int32_t n_new,
+                                           int32_t num_q_heads) {
+  if (!ring || n_new <= 0 || num_q_heads <= 0 || ring->head_dim <= 0) return 0;
+  return fp8_layout(ring, n_new, num_q_heads).bytes;
+}
+
+frt_status frt_stream_attn_step_fp8(const frt_ring *ring, const frt_fp8_scales *scales,
+                                    const frt_rope *rope, const frt_mask *mask, const void *q,
+                                    const void *k_new, const void *v_new, int32_t n_new,
+                                    int32_t num_q_heads, float softmax_scale, void *workspace,
+                                    size_t workspace_bytes, void *out, float *lse, void *stream) {
+  frt_status s;
+  if ((s = check_ring(ring)) != FRT_OK) return s;
+  if ((s = check_scales(scales)) != FRT_OK) return s;
+  if (ring->head_dim != 128)
+    return fail(FRT_ERR_UNSUPPORTED, "FP8 attention supports head_dim 128 (got %d)",
+                ring->head_dim);
+  if ((s = check_rope(rope, ring->head_dim)) != FRT_OK) return s;
+  if ((s = check_mask(mask, ring->capacity)) != FRT_OK) return s;
+  if (num_q_heads < 1 || num_q_heads % ring->num_kv_heads)
+    return fail(FRT_ERR_SHAPE, "num_q_heads=%d is not a multiple of num_kv_heads=%d", num_q_heads,
+                ring->num_kv_heads);
+  if (n_new < 0) return fail(FRT_ERR_SHAPE, "n_new=%d < 0", n_new);
+  if (n_new > ring->capacity)
+    return fail(FRT_ERR_CAPACITY, "n_new=%d > capacity=%d", n_new, ring->capacity);
+  if (n_new == 0) return FRT_OK;
+  const int G = num_q_heads / ring->num_kv_heads;
+  if ((size_t)n_new * G * ring->head_dim >= (size_t)1 << 31)
+    return fail(FRT_ERR_SHAPE, "n_new*G*head_dim must be below 2^31");
+  if ((s = check_io(q, "q")) != FRT_OK) return s;
+  if ((s = check_io(k_new, "k_new")) != FRT_OK) return s;
+  if ((s = check_io(v_new, "v_new")) != FRT_OK) return s;
+  if ((s = check_io(out, "out")) != FRT_OK) return s;
+  if (lse && !aligned(lse, 4)) return fail(FRT_ERR_ALIGN, "lse must be 4-byte aligned");
+  const Fp8Layout lay = fp8_layout(ring, n_new, num_q_heads);
+  if (!workspace) return fail(FRT_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", lay.bytes);
+  if (workspace_bytes < lay.bytes)
+    return fail(FRT_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, lay.bytes);
+  if (!aligned(workspace, 256)) return fail(FRT_ERR_ALIGN, "workspace must be 256-byte aligned");
+
+  char *ws = static_cast<char *>(workspace);
+  PrepFp8Params pp;
+  pp.q = static_cast<const uint16_t *>(q);
+  pp.k_new = static_cast<const uint16_t *>(k_new);
+  pp.v_new = static_cast<const uint16_t *>(v_new);
+  pp.seq_len = ring->seq_len;
+  pp.qr = reinterpret_cast<uint8_t *>(ws + lay.q_off);
+  pp.qs = reinterpret_cast<float *>(ws + lay.s_off);
+  pp.kr = reinterpret_cast<uint8_t *>(ws + lay.k_off);
+  pp.vt = reinterpret_cast<uint8_t *>(ws + lay.v_off);
+  pp.sc.k = scales->k_scale;
+  pp.sc.v = scales->v_scale;
+  pp.B = ring->num_streams;
+  pp.Hq = num_q_heads;
+  pp.Hkv = ring->num_kv_heads;
+  pp.G = G;
+  pp.D = ring->head_dim;
+  pp.n = n_new;
+  pp.n_pad = lay.n_pad;
+  pp.qmul = q_multiplier(softmax_scale, ring->head_dim);
+
+  AttnFp8Params ap;
+  ap.qr = pp.qr;
+  ap.qs = pp.qs;
+  ap.kr = pp.kr;
+  ap.vt = pp.vt;
+  ap.k_ring = static_cast<const uint8_t *>(ring->k_ring);
+  ap.v_ring = static_cast<const uint8_t *>(ring->v_ring);
+  ap.seq_len = ring->seq_len;
+  ap.sc = pp.sc;
+  ap.out = static_cast<uint16_t *>(out);
+  ap.lse = lse;
+  ap.B = pp.B;
+  ap.Hq = num_q_heads;
+  ap.Hkv = pp.Hkv;
+  ap.G = G;
+  ap.n = n_new;
+  ap.n_pad = lay.n_pad;
+  ap.C = ring->capacity;
+  ap.mask_kind = mask->kind;
+  ap.mask_block = mask->block;
+  ap.mask_window = mask->window;
+  ap.row_tiles = (n_new * G + kChunkRows - 1) / kChunkRows;
+
+  const RopeDev rd = rope_dev(rope);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if ((s = launch("chunk_prep", st, [&] { return launch_chunk_prep_fp8(pp, rd, st); })) != FRT_OK)
+    return s;
+  return launch("chunk_attn", st, [&] { return launch_chunk_attn_fp8(ap, ring->head_dim, st); });
+}
+
 int32_t frt_decode_max_splits(const frt_ring *ring) {
   if (!ring || ring->capacity <= 0 || ring->num_streams <= 0 || ring->num_kv_heads <= 0) return 0;
   return decode_piece_waves(ring->num_streams, ring->num_kv_heads, ring->capacity);

@@ -29,6 +29,47 @@ struct ChunkAppendParams {
   int B, Hkv, D, C, n, n_pad;
 };
 
+// FP8 (e4m3fn) ring: same layouts as the bf16 ring with one-byte elements;
+// per-(stream, KV head) fp32 scales, a stored code standing for code * scale.
+struct Fp8Scales {
+  const float *k, *v;     // [B][Hkv]
+};
+
+struct AppendFp8Params {
+  const uint16_t *k_new;  // [B][n][Hkv][D]  bf16
+  const uint16_t *v_new;
+  uint8_t *k_ring;        // [B][Hkv][C][D]
+  uint8_t *v_ring;        // [B][Hkv][C*D]   32-slot blocks
+  int64_t *seq_len;
+  Fp8Scales sc;
+  int B, Hkv, D, C, n;
+};
+
+struct PrepFp8Params {
+  const uint16_t *q, *k_new, *v_new;
+  const int64_t *seq_len;
+  uint8_t *qr;            // [B][Hkv][n*G][D]  query codes
+  float *qs;              // [B][Hkv][n*G]     their row scale 2^e
+  uint8_t *kr;            // [B][Hkv][n_pad][D] own key codes (as the ring stores them)
+  uint8_t *vt;            // [B][Hkv][n_pad*D]  own value codes, ring block layout
+  Fp8Scales sc;
+  int B, Hq, Hkv, G, D, n, n_pad;
+  double qmul;
+};
+
+struct AttnFp8Params {
+  const uint8_t *qr, *kr, *vt;
+  const float *qs;
+  const uint8_t *k_ring, *v_ring;
+  const int64_t *seq_len;
+  Fp8Scales sc;
+  uint16_t *out;
+  float *lse;
+  int B, Hq, Hkv, G, n, n_pad, C;
+  int mask_kind, mask_block, mask_window;
+  int row_tiles;
+};
+
 struct PrepParams {
   const uint16_t *q;      // [B][n][Hq][D]
   const uint16_t *k_new;  // [B][n][Hkv][D]
@@ -102,6 +143,9 @@ hipError_t launch_seq_advance(int64_t *seq_len, int B, int n, hipStream_t s);
 hipError_t launch_chunk_prep(const PrepParams &p, const RopeDev &r, hipStream_t s);
 hipError_t launch_chunk_attn(const AttnParams &p, int D, hipStream_t s);
 hipError_t launch_chunk_append(const ChunkAppendParams &p, hipStream_t s);
+hipError_t launch_rope_append_fp8(const AppendFp8Params &p, const RopeDev &r, hipStream_t s);
+hipError_t launch_chunk_prep_fp8(const PrepFp8Params &p, const RopeDev &r, hipStream_t s);
+hipError_t launch_chunk_attn_fp8(const AttnFp8Params &p, int D, hipStream_t s);
 hipError_t launch_decode_split(const DecodeParams &p, const RopeDev &r, hipStream_t s);
 hipError_t launch_decode_combine(const DecodeParams &p, hipStream_t s);
 

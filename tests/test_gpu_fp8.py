@@ -1,0 +1,156 @@
+"""FP8 (e4m3fn) ring append and step attention on the GPU against the FP8
+oracle: ring bytes bit for bit, attention outputs within tolerance."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import fp8
+import paper_2607_18171_amd as frt
+from workloads import (WORKLOADS, RopeSpec, MaskSpec, ROPE_3D, MASK_BLOCK_CAUSAL, MASK_CAUSAL,
+                       make_case, shrink)
+from gpu_helpers import to_dev, from_dev, bf16_dev_to_f64, gpu_rope, gpu_mask
+
+pytestmark = pytest.mark.gpu
+
+
+def scales(wl, seed):
+    """Per-(stream, KV head) scales putting N(0, 1)-sized values well inside +-448."""
+    rng = np.random.default_rng(100 + seed)
+    ks = rng.uniform(0.01, 0.04, (wl.B, wl.Hkv)).astype(np.float32) * wl.qk_scale
+    vs = rng.uniform(0.01, 0.04, (wl.B, wl.Hkv)).astype(np.float32)
+    return ks, vs
+
+
+def build_fp8_rings(case, ks, vs, extra_tokens=0):
+    wl = case.wl
+    max_tok = int(case.prior_lengths.max()) + wl.n + extra_tokens + 1
+    rope = gpu_rope(wl, max_tok)
+    ring = frt.RingFp8(wl.B, wl.Hkv, wl.d, wl.C, torch.from_numpy(ks), torch.from_numpy(vs))
+    oring = fp8.RingFP8(wl.B, wl.Hkv, wl.C, wl.d)
+    for k, v in case.prior_steps:
+        frt.kv_append_fp8(ring, rope, to_dev(k), to_dev(v))
+        fp8.kv_append_fp8(oring, k, v, wl.rope, ks, vs)
+    for b, (k, v) in enumerate(case.prior_fills):
+        n = k.shape[1]
+        for s in range(0, n, wl.C):
+            e = min(n, s + wl.C)
+            frt.kv_append_fp8(ring.view_stream(b), rope, to_dev(k[:, s:e]), to_dev(v[:, s:e]))
+            fp8.kv_append_fp8(oring, k[:, s:e], v[:, s:e], wl.rope, ks, vs, streams=[b])
+    return ring, oring, rope
+
+
+def ring_codes_equal(ring, oring):
+    k = ring.k.cpu().numpy()
+    v = ring.v[:, :, ring.v_index().reshape(-1)].reshape(ring.B, ring.Hkv, ring.C, ring.d)
+    return (np.array_equal(k, oring.k) and np.array_equal(v.cpu().numpy(), oring.v)
+            and np.array_equal(ring.seq_len.cpu().numpy(), oring.seq_len))
+
+
+def run_fp8_step(case, ring, rope, rows_lse=True):
+    wl = case.wl
+    q, k, v = to_dev(case.q), to_dev(case.k_new), to_dev(case.v_new)
+    out = torch.empty_like(q)
+    lse = torch.empty((wl.B, wl.Hq, wl.n), dtype=torch.float32, device="cuda")
+    ws = torch.empty(frt.stream_attn_fp8_workspace_bytes(ring, wl.n, wl.Hq), dtype=torch.uint8,
+                     device="cuda")
+    frt.stream_attn_step_fp8(ring, rope, gpu_mask(wl), q, k, v, out, ws, lse=lse)
+    torch.cuda.synchronize()
+    return out, lse
+
+
+SMALL = {
+    "video_small": shrink(WORKLOADS["video_1p3b"], Hq=2, Hkv=2, n=72, C=288,
+                          rope=RopeSpec(ROPE_3D, (44, 42, 42), (4, 6)),
+                          mask=MaskSpec(MASK_BLOCK_CAUSAL, 72, 4), prior_steps=6),
+    # unit-variance Q and K: see the note on the tolerance below
+    "video_vpart": shrink(WORKLOADS["video_14b"], Hq=2, Hkv=2, n=40, C=240,
+                          rope=RopeSpec(ROPE_3D, (44, 42, 42), (2, 4)),
+                          mask=MaskSpec(MASK_BLOCK_CAUSAL, 40, 6), prior_steps=9,
+                          qk_scale=1.0),
+    "gqa_swa": shrink(WORKLOADS["prefill_swa"], B=3, Hq=8, Hkv=2, n=100, C=256,
+                      mask=MaskSpec(MASK_CAUSAL, 0, 200), len_lo=0, len_hi=800),
+    "mha_causal": shrink(WORKLOADS["prefill_swa"], B=2, Hq=4, Hkv=4, n=37, C=512,
+                         mask=MaskSpec(MASK_CAUSAL, 0, 0), len_lo=0, len_hi=400),
+}
+
+# Error sources between the kernel and the FP8 oracle: fp32 accumulation of
+# the exact code products, the hardware exp2, and so the rare weight whose
+# exact value lies within that error of a rounding boundary of the code (one
+# code step is 1/8 to 1/16 of the weight); bf16 rounding of the output. And
+# one of definition: the oracle codes weights against m = ceil(row max), the
+# kernel against its running integer max, at most one below it between
+# raises, so only weights in the subnormal codes (2^-13 of the largest and
+# less) can round differently; on the full-size 14B-like step (32760 keys of
+# 3x unit logits, the widest spread of mass here) that is 0.5% of max|V| at
+# most and 3e-4 on average.
+MAX_REL_V = 1e-2   # of max |v_scale * value(code)| over the visible values
+MEAN_ABS = 1e-3
+
+
+def vmax_fp8(oring, case, vs):
+    wl = case.wl
+    vals = [np.abs(fp8.e4m3_decode(fp8.stored_v8(case.v_new[b, :, h, :], vs[b, h])) * vs[b, h]).max()
+            for b in range(wl.B) for h in range(wl.Hkv)]
+    vals.append(max(np.abs(fp8.e4m3_decode(oring.v[b, h]) * vs[b, h]).max()
+                    for b in range(wl.B) for h in range(wl.Hkv)))
+    return float(max(vals))
+
+
+def check_fp8(got, ref, vmax, what):
+    err = np.abs(got - ref)
+    assert np.all(np.isfinite(got)), what
+    mx, mean = float(err.max()), float(err.mean())
+    print("%s: max|err| %.3g (%.3g of max|V|) mean %.3g" % (what, mx, mx / vmax, mean))
+    assert mx <= MAX_REL_V * vmax, "%s: max|err| %.3g > %.3g" % (what, mx, MAX_REL_V * vmax)
+    assert mean <= MEAN_ABS, "%s: mean|err| %.3g" % (what, mean)
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_fp8_append_codes_match_oracle(name):
+    wl = SMALL[name]
+    case = make_case(wl, 0)
+    ks, vs = scales(wl, 0)
+    ring, oring, rope = build_fp8_rings(case, ks, vs)
+    assert ring_codes_equal(ring, oring)
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+@pytest.mark.parametrize("seed", [0, 1])
+def test_fp8_attention_small(name, seed):
+    wl = SMALL[name]
+    case = make_case(wl, seed)
+    ks, vs = scales(wl, seed)
+    ring, oring, rope = build_fp8_rings(case, ks, vs)
+    out, lse = run_fp8_step(case, ring, rope)
+    ref, ref_lse = fp8.stream_attn_fp8(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask,
+                                       ks, vs)
+    check_fp8(bf16_dev_to_f64(out), ref, vmax_fp8(oring, case, vs), name)
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() < 2e-2
+    assert ring_codes_equal(ring, oring)  # attention reads the ring only
+
+
+@pytest.mark.parametrize("name", ["video_1p3b", "video_14b"])
+def test_fp8_attention_full_size_sampled_rows(name):
+    wl = WORKLOADS[name]
+    case = make_case(wl, 0)
+    ks, vs = scales(wl, 0)
+    ring, oring, rope = build_fp8_rings(case, ks, vs)
+    out, lse = run_fp8_step(case, ring, rope)
+    rng = np.random.default_rng(3)
+    rows = np.unique(np.concatenate([[0, 255, 256, wl.n - 1], rng.integers(0, wl.n, 12)]))
+    ref, ref_lse = fp8.stream_attn_fp8(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask,
+                                       ks, vs, rows=rows)
+    check_fp8(bf16_dev_to_f64(out)[:, rows], ref[:, rows], vmax_fp8(oring, case, vs), name)
+    assert np.abs(lse.cpu().numpy()[:, :, rows] - ref_lse[:, :, rows]).max() < 2e-2
+
+
+def test_fp8_attention_rejects_head_dim_64():
+    wl = shrink(WORKLOADS["prefill_swa"], B=1, Hq=2, Hkv=1, d=64, n=8, C=64,
+                rope=RopeSpec(0), mask=MaskSpec(MASK_CAUSAL, 0, 0), len_lo=8, len_hi=8)
+    case = make_case(wl, 0)
+    ks, vs = scales(wl, 0)
+    ring, oring, rope = build_fp8_rings(case, ks, vs)
+    assert ring_codes_equal(ring, oring)  # the append supports head_dim 64
+    with pytest.raises(frt.FrtError):
+        run_fp8_step(case, ring, rope)

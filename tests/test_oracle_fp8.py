@@ -189,7 +189,7 @@ def _twin(ring, q, k_new, v_new, rope, mask, ks, vs):
                         s = 2.0 ** e * sk * sum(qv[t] * kv[t] for t in range(d))
                         scored.append((s, vv))
                 m = math.ceil(max(s for s, _ in scored))
-                w = [values[enc(2.0 ** (s - m))] for s, _ in scored]
+                w = [values[enc(2.0 ** (s - m + 7))] for s, _ in scored]
                 tot = sum(w)
                 for t in range(d):
                     out[b, i, hq, t] = sv * sum(wk * vv[t] for wk, (_, vv) in zip(w, scored)) / tot
@@ -213,3 +213,31 @@ def test_vectorised_matches_loop_twin(rope, mask, B, Hq, Hkv, C, steps, n):
     out, _ = fp8.stream_attn_fp8(ring, q, k, v, rope, mask, ks, vs)
     ref = _twin(ring, q, k, v, rope, mask, ks, vs)
     assert np.allclose(out, ref, rtol=0, atol=1e-12)
+
+
+def test_spread_mass_stays_in_normal_codes():
+    """One key 12 powers of two above N others: the others' weights are the
+    normal code 2^-5 against 2^7 for the top key (a coding relative to the
+    top key alone would flush them to zero)."""
+    rope = RopeSpec(ROPE_NONE)
+    mask = MaskSpec(MASK_CAUSAL, 0, 0)
+    d, N = 16, 20
+    ks = np.ones((1, 1), np.float32)
+    vs = np.ones((1, 1), np.float32)
+    ring = fp8.RingFP8(1, 1, 32, d)
+    k = np.zeros((1, N + 1, 1, d), np.uint16)
+    k[0, 0, 0, :] = 0x4000  # bf16 2.0: its code is 2.0
+    rng = np.random.default_rng(6)
+    v = rand_bits(rng, (1, N + 1, 1, d))
+    fp8.kv_append_fp8(ring, k, v, rope, ks, vs)
+    # query 1.0 everywhere: a = scale*log2(e) = 0.3607 -> e = -10, code 384, so
+    # the top score is 2^-10 * 384 * 16 * 2.0 = 12 and the others 0
+    q = np.full((1, 1, 1, d), 0x3f80, np.uint16)
+    out, lse = fp8.stream_attn_fp8(ring, q, np.zeros((1, 1, 1, d), np.uint16),
+                                   np.zeros((1, 1, 1, d), np.uint16), rope, mask, ks, vs)
+    V = fp8.e4m3_decode(ring.v[0, 0, :N + 1])
+    Vown = np.zeros(d)  # the step's own key is zero, its value zero: weight 2^-5
+    w = np.array([128.0] + [2.0 ** -5] * N + [2.0 ** -5])
+    want = (w[:, None] * np.vstack([V, Vown])).sum(axis=0) / w.sum()
+    assert np.allclose(out[0, 0, 0], want, rtol=0, atol=1e-12)
+    assert abs(lse[0, 0, 0] - math.log(2.0 ** 12 + N + 1)) < 1e-9
