@@ -35,6 +35,7 @@ from workloads import WORKLOADS, make_case, MASK_BLOCK_CAUSAL, MASK_CAUSAL  # no
 
 METRIC = "attention TFLOP/s + % bf16 MFMA peak per streaming step; decode HBM GB/s"
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA (published 2.5 PFLOP/s)
+PEAK_FP8_TFLOPS = 5033.2    # MI355X dense fp8 MFMA (published 5.0 PFLOP/s)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published 8 TB/s)
 
 
@@ -77,26 +78,49 @@ def _blas_threads() -> int:
         return len(os.sched_getaffinity(0))
 
 
-def cpu_baseline(wl, case, seconds: float):
+def fp8_scales(wl):
+    """Per-(stream, KV head) FP8 scales: N(0, 1)*qk_scale keys and N(0, 1)
+    values land around code 50, their tails well inside +-448."""
+    ks = np.full((wl.B, wl.Hkv), 0.02 * wl.qk_scale, np.float32)
+    vs = np.full((wl.B, wl.Hkv), 0.02, np.float32)
+    return ks, vs
+
+
+def cpu_baseline(wl, case, seconds: float, fp8: bool = False):
     """Time the fp64 oracle on a bounded sample of the measured step.
 
     The sample is the first `rows` query tokens of every stream and head; `rows`
     grows from 64 until one timed call takes at least half of `seconds` (or
-    covers the whole chunk). The last call is the one reported.
+    covers the whole chunk). The last call is the one reported. With fp8 the
+    oracle is the FP8 step's.
     """
     import oracle
-    oring = oracle.new_ring(wl.B, wl.Hkv, wl.C, wl.d)
+    from oracle import fp8 as ofp8
+    if fp8:
+        ks, vs = fp8_scales(wl)
+        oring = ofp8.RingFP8(wl.B, wl.Hkv, wl.C, wl.d)
+        app = lambda r, k, v, streams=None: ofp8.kv_append_fp8(r, k, v, wl.rope, ks, vs,  # noqa
+                                                               streams=streams)
+    else:
+        oring = oracle.new_ring(wl.B, wl.Hkv, wl.C, wl.d)
+        app = lambda r, k, v, streams=None: oracle.kv_append(r, k, v, wl.rope,  # noqa
+                                                             streams=streams)
     for k, v in case.prior_steps:
-        oring = oracle.kv_append(oring, k, v, wl.rope)
+        oring = app(oring, k, v)
     for b, (k, v) in enumerate(case.prior_fills):
         for s in range(0, k.shape[1], wl.C):
             e = min(k.shape[1], s + wl.C)
-            oring = oracle.kv_append(oring, k[:, s:e], v[:, s:e], wl.rope, streams=[b])
+            oring = app(oring, k[:, s:e], v[:, s:e], streams=[b])
 
     def timed(nrows):
         rows = np.arange(min(wl.n, nrows), dtype=np.int64)
         t0 = time.perf_counter()
-        oracle.stream_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask, rows=rows)
+        if fp8:
+            ofp8.stream_attn_fp8(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask, ks, vs,
+                                 rows=rows)
+        else:
+            oracle.stream_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask,
+                               rows=rows)
         return rows, time.perf_counter() - t0
 
     rows, dt = timed(64)
@@ -141,9 +165,11 @@ def cpu_baseline_decode(wl, case, seconds: float):
 # WRITE_SIZE passes scaled by a plain-copy calibration; used only while the
 # kernel's sources still hash to what the counters were taken on.
 TRAFFIC_FILES = {("chunk_attn", "video_1p3b"): "profiles/chunk_attn_video_1p3b.txt",
-                 ("decode_split", "decode"): "profiles/decode_split_decode.txt"}
+                 ("decode_split", "decode"): "profiles/decode_split_decode.txt",
+                 ("chunk_attn_fp8", "video_1p3b"): "profiles/chunk_attn_fp8_video_1p3b.txt"}
 KERNEL_SOURCES = {"chunk_attn": ["paper_2607_18171_amd/csrc/frt_attn.hip"],
-                  "decode_split": ["paper_2607_18171_amd/csrc/frt_decode.hip"]}
+                  "decode_split": ["paper_2607_18171_amd/csrc/frt_decode.hip"],
+                  "chunk_attn_fp8": ["paper_2607_18171_amd/csrc/frt_fp8_attn.hip"]}
 COMMON_SOURCES = ["paper_2607_18171_amd/csrc/frt_device.hpp",
                   "paper_2607_18171_amd/csrc/frt_launch.hpp", "paper_2607_18171_amd/build.py"]
 
@@ -176,6 +202,9 @@ def main(argv=None):
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target length of the oracle's timed CPU sample (0 = skip)")
+    ap.add_argument("--fp8", action="store_true",
+                    help="the FP8 (e4m3fn) ring and step attention (chunk workloads, head_dim "
+                         "128): frt_stream_attn_step_fp8 then frt_kv_append_fp8")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized device buffer 3 times (known HBM traffic for "
                          "scaling FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -199,6 +228,9 @@ def main(argv=None):
     import paper_2607_18171_amd as frt
 
     wl = WORKLOADS[args.workload]
+    if args.fp8 and (wl.n == 1 or wl.d != 128):
+        print("--fp8 covers the chunk workloads with head_dim 128", file=sys.stderr)
+        return 2
     case = make_case(wl, args.seed)
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
@@ -211,19 +243,28 @@ def main(argv=None):
     max_tokens = int(case.prior_lengths.max()) + (total_steps + 1) * wl.n + 1
     rope = frt.Rope.for_tokens(wl.rope.mode, wl.rope.axis_dims, wl.rope.frame_hw, max_tokens,
                                wl.rope.base)
-    ring = frt.Ring(wl.B, wl.Hkv, wl.d, wl.C)
+    if args.fp8:
+        ks, vs = fp8_scales(wl)
+        ring = frt.RingFp8(wl.B, wl.Hkv, wl.d, wl.C, torch.from_numpy(ks), torch.from_numpy(vs))
+        append = frt.kv_append_fp8
+    else:
+        ring = frt.Ring(wl.B, wl.Hkv, wl.d, wl.C)
+        append = frt.kv_append
     for k, v in case.prior_steps:
-        frt.kv_append(ring, rope, to_dev(k), to_dev(v))
+        append(ring, rope, to_dev(k), to_dev(v))
     for b, (k, v) in enumerate(case.prior_fills):
         for s in range(0, k.shape[1], wl.C):
             e = min(k.shape[1], s + wl.C)
-            frt.kv_append(ring.view_stream(b), rope, to_dev(k[:, s:e]), to_dev(v[:, s:e]))
+            append(ring.view_stream(b), rope, to_dev(k[:, s:e]), to_dev(v[:, s:e]))
     q, kn, vn = to_dev(case.q), to_dev(case.k_new), to_dev(case.v_new)
     out = torch.empty_like(q)
     msk = frt.mask(wl.mask.kind, wl.mask.block, wl.mask.window)
     decode = wl.n == 1
     if decode:
         ws = torch.empty(frt.decode_workspace_bytes(ring, wl.Hq), dtype=torch.uint8, device=dev)
+    elif args.fp8:
+        ws = torch.empty(frt.stream_attn_fp8_workspace_bytes(ring, wl.n, wl.Hq),
+                         dtype=torch.uint8, device=dev)
     else:
         ws = torch.empty(frt.stream_attn_workspace_bytes(ring, wl.n, wl.Hq), dtype=torch.uint8,
                          device=dev)
@@ -232,6 +273,9 @@ def main(argv=None):
     def step():
         if decode:  # attention and the one-token append in one call
             frt.decode_step(ring, rope, msk, q, kn, vn, out, ws)
+        elif args.fp8:
+            frt.stream_attn_step_fp8(ring, rope, msk, q, kn, vn, out, ws)
+            frt.kv_append_fp8(ring, rope, kn, vn)
         else:
             frt.stream_step(ring, rope, msk, q, kn, vn, out, ws)
 
@@ -290,20 +334,23 @@ def main(argv=None):
         unit = "TFLOP/s"
         dom = kernels["chunk_attn"]
         achieved = kflops_step / (dom["avg_us"] * 1e-6) / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                "traffic": recorded_traffic("chunk_attn", wl.name), "kernel": "chunk_attn"}
+        peak = PEAK_FP8_TFLOPS if args.fp8 else PEAK_BF16_TFLOPS  # the contraction's own dtype
+        kname = "chunk_attn_fp8" if args.fp8 else "chunk_attn"
+        roof = {"bound": "mfma", "achieved": achieved, "peak": peak,
+                "unit": "TFLOP/s", "frac": achieved / peak,
+                "traffic": recorded_traffic(kname, wl.name), "kernel": kname}
 
     cpu = None
     if args.cpu_seconds > 0 and not decode:
-        cpu = cpu_baseline(wl, case, args.cpu_seconds)
+        cpu = cpu_baseline(wl, case, args.cpu_seconds, fp8=args.fp8)
     elif args.cpu_seconds > 0:
         cpu = cpu_baseline_decode(wl, case, args.cpu_seconds)
 
     line = {
         "metric": METRIC, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "scaling": "weak", "vs_baseline": None, "dtype": "fp8" if args.fp8 else "bf16",
+        "data": "synthetic",
         "config": {"workload": wl.name, "streams": wl.B, "q_heads": wl.Hq, "kv_heads": wl.Hkv,
                    "head_dim": wl.d, "chunk_tokens": wl.n, "ring_slots": wl.C,
                    "mask": "block_causal" if wl.mask.kind == MASK_BLOCK_CAUSAL else "causal",
