@@ -169,7 +169,8 @@ TRAFFIC_FILES = {("chunk_attn", "video_1p3b"): "profiles/chunk_attn_video_1p3b.t
                  ("chunk_attn_fp8", "video_1p3b"): "profiles/chunk_attn_fp8_video_1p3b.txt"}
 KERNEL_SOURCES = {"chunk_attn": ["paper_2607_18171_amd/csrc/frt_attn.hip"],
                   "decode_split": ["paper_2607_18171_amd/csrc/frt_decode.hip"],
-                  "chunk_attn_fp8": ["paper_2607_18171_amd/csrc/frt_fp8_attn.hip"]}
+                  "chunk_attn_fp8": ["paper_2607_18171_amd/csrc/frt_fp8_attn.hip",
+                                     "paper_2607_18171_amd/csrc/frt_fp8.hpp"]}
 COMMON_SOURCES = ["paper_2607_18171_amd/csrc/frt_device.hpp",
                   "paper_2607_18171_amd/csrc/frt_launch.hpp", "paper_2607_18171_amd/build.py"]
 

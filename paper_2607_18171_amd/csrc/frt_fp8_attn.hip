@@ -24,6 +24,7 @@
 // Scores: the MFMA gives q8 . k8; the score in base-2 units is that times
 // 2^e_row * s_k (exact scaling by a power of two, then the key scale), folded
 // into the fma that subtracts the reference max before exp2.
+#include "frt_fp8.hpp"
 #include "frt_launch.hpp"
 
 namespace frt {
@@ -380,7 +381,7 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_fp8_kernel(AttnFp8Params p
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
         const int r = 4 * w;
-        pf[4 * kb + w] = (int)e4m3x4(__builtin_amdgcn_exp2f(fmaf(s[kb][r], cq, nm)),
+        pf[4 * kb + w] = (int)e4m3x4_inrange(__builtin_amdgcn_exp2f(fmaf(s[kb][r], cq, nm)),
                                      __builtin_amdgcn_exp2f(fmaf(s[kb][r + 1], cq, nm)),
                                      __builtin_amdgcn_exp2f(fmaf(s[kb][r + 2], cq, nm)),
                                      __builtin_amdgcn_exp2f(fmaf(s[kb][r + 3], cq, nm)));

@@ -7,6 +7,7 @@
 // base-2 score units (rotated and multiplied by scale*log2(e) in double,
 // rounded to float) and coded with a power-of-two scale per query row, the
 // smallest 2^e with max|a| <= 448 * 2^e, so that the division is exact.
+#include "frt_fp8.hpp"
 #include "frt_launch.hpp"
 
 namespace frt {
@@ -132,9 +133,9 @@ __global__ __launch_bounds__(256) void chunk_prep_fp8_kernel(PrepFp8Params p, Ro
 #pragma unroll
     for (int j = 0; j < 8; ++j) sa[j] = ldexpf(a[j], -e);
     const size_t row = head * (size_t)p.n * G + (size_t)i * G + g;
-    u32x2 qc;
-    qc[0] = e4m3x4(sa[0], sa[1], sa[2], sa[3]);
-    qc[1] = e4m3x4(sa[4], sa[5], sa[6], sa[7]);
+    u32x2 qc;  // |sa| <= 448 by the choice of e
+    qc[0] = e4m3x4_inrange(sa[0], sa[1], sa[2], sa[3]);
+    qc[1] = e4m3x4_inrange(sa[4], sa[5], sa[6], sa[7]);
     *reinterpret_cast<u32x2 *>(p.qr + row * D + c * 8) = qc;
     if (c == 0) p.qs[row] = ldexpf(1.f, e);
   }
