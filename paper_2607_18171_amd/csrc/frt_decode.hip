@@ -232,9 +232,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecWavesPe
   {
     const StreamTiles st = stream_tiles(p, b);
     const int pc = (st.n + per - 1) / per;  // pieces per KV head of this stream
-    const int kvh = (int)((wv - Kb) / pc);
-    const int j0 = (int)((wv - Kb) % pc) * per;
-    const int cnt = min(st.n - j0, per);
+    // The piece is the same in every lane (it comes from a ballot, shuffles
+    // and per-stream values); stating it keeps its descriptors scalar and its
+    // tile branches uniform: a descriptor the compiler takes for divergent
+    // costs a readfirstlane loop per load.
+    const int kvh = uniform_i32((int)((wv - Kb) / pc));
+    const int j0 = uniform_i32((int)((wv - Kb) % pc) * per);
+    const int cnt = uniform_i32(min(st.n - j0, per));
     u32x4 kraw[kDecBufs][2][NKS];
     u32x4 vraw[kDecBufs][NDB];
     bf16x8 qf[NKS];
