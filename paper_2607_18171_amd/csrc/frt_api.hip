@@ -34,6 +34,17 @@ bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // ---------------------------------------------------------------- timing --
+}  // namespace
+
+namespace frt {
+DispatchEvents &pending_dispatch_events() {
+  thread_local DispatchEvents ev;
+  return ev;
+}
+}  // namespace frt
+
+namespace {
+
 struct TimingRec {
   const char *name;
   hipEvent_t start, stop;
@@ -65,12 +76,23 @@ frt_status launch(const char *name, hipStream_t s, F &&f) {
       b = take_event();
     }
   }
-  if (a) (void)hipEventRecord(a, s);
+  if (a && b) pending_dispatch_events() = DispatchEvents{a, b};
   hipError_t e = f();
-  if (b) (void)hipEventRecord(b, s);
+  // the dispatch takes the events; a launcher that failed before it did not
+  const bool taken = pending_dispatch_events().start == nullptr;
+  pending_dispatch_events() = DispatchEvents{};
   if (a && b) {
     std::lock_guard<std::mutex> lk(g_tmu);
-    g_recs.push_back({name, a, b});
+    if (taken && e == hipSuccess) {
+      g_recs.push_back({name, a, b});
+    } else {
+      g_pool.push_back(a);
+      g_pool.push_back(b);
+    }
+  } else {
+    std::lock_guard<std::mutex> lk(g_tmu);
+    if (a) g_pool.push_back(a);
+    if (b) g_pool.push_back(b);
   }
   if (e != hipSuccess) return fail(FRT_ERR_HIP, "%s launch failed: %s", name, hipGetErrorString(e));
   return FRT_OK;

@@ -202,40 +202,40 @@ __global__ __launch_bounds__(256) void chunk_append_kernel(ChunkAppendParams p) 
 hipError_t launch_chunk_append(const ChunkAppendParams &p, hipStream_t s) {
   dim3 grid((p.n + kAppendTokens - 1) / kAppendTokens, p.Hkv, p.B);
   if (p.D == 128)
-    hipLaunchKernelGGL(chunk_append_kernel<128>, grid, dim3(256), 0, s, p);
+    dispatch(chunk_append_kernel<128>, grid, dim3(256), s, p);
   else
-    hipLaunchKernelGGL(chunk_append_kernel<64>, grid, dim3(256), 0, s, p);
+    dispatch(chunk_append_kernel<64>, grid, dim3(256), s, p);
   return hipGetLastError();
 }
 
 hipError_t launch_rope_append(const AppendParams &p, const RopeDev &r, hipStream_t s) {
   dim3 grid((p.n + kAppendTokens - 1) / kAppendTokens, p.Hkv, p.B);
   if (p.D == 128)
-    hipLaunchKernelGGL(rope_append_kernel<128>, grid, dim3(256), 0, s, p, r);
+    dispatch(rope_append_kernel<128>, grid, dim3(256), s, p, r);
   else
-    hipLaunchKernelGGL(rope_append_kernel<64>, grid, dim3(256), 0, s, p, r);
+    dispatch(rope_append_kernel<64>, grid, dim3(256), s, p, r);
   return hipGetLastError();
 }
 
 hipError_t launch_rope_append_small(const AppendParams &p, const RopeDev &r, hipStream_t s) {
   if (p.D == 128)
-    hipLaunchKernelGGL(rope_append_small_kernel<128>, dim3(p.B), dim3(256), 0, s, p, r);
+    dispatch(rope_append_small_kernel<128>, dim3(p.B), dim3(256), s, p, r);
   else
-    hipLaunchKernelGGL(rope_append_small_kernel<64>, dim3(p.B), dim3(256), 0, s, p, r);
+    dispatch(rope_append_small_kernel<64>, dim3(p.B), dim3(256), s, p, r);
   return hipGetLastError();
 }
 
 hipError_t launch_seq_advance(int64_t *seq_len, int B, int n, hipStream_t s) {
-  hipLaunchKernelGGL(seq_advance_kernel, dim3((B + 255) / 256), dim3(256), 0, s, seq_len, B, n);
+  dispatch(seq_advance_kernel, dim3((B + 255) / 256), dim3(256), s, seq_len, B, n);
   return hipGetLastError();
 }
 
 hipError_t launch_chunk_prep(const PrepParams &p, const RopeDev &r, hipStream_t s) {
   dim3 grid((p.n_pad + kAppendTokens - 1) / kAppendTokens, p.Hkv, p.B);
   if (p.D == 128)
-    hipLaunchKernelGGL(chunk_prep_kernel<128>, grid, dim3(256), 0, s, p, r);
+    dispatch(chunk_prep_kernel<128>, grid, dim3(256), s, p, r);
   else
-    hipLaunchKernelGGL(chunk_prep_kernel<64>, grid, dim3(256), 0, s, p, r);
+    dispatch(chunk_prep_kernel<64>, grid, dim3(256), s, p, r);
   return hipGetLastError();
 }
 

@@ -485,9 +485,9 @@ hipError_t launch_chunk_attn(const AttnParams &p, int D, hipStream_t s) {
   dim3 grid((nlog + 7) / 8 * 8);
   dim3 block(kChunkWaves * 64);
   if (D == 128)
-    hipLaunchKernelGGL((chunk_attn_kernel<128, kChunkWaves>), grid, block, 0, s, p);
+    dispatch((chunk_attn_kernel<128, kChunkWaves>), grid, block, s, p);
   else
-    hipLaunchKernelGGL((chunk_attn_kernel<64, kChunkWaves>), grid, block, 0, s, p);
+    dispatch((chunk_attn_kernel<64, kChunkWaves>), grid, block, s, p);
   return hipGetLastError();
 }
 

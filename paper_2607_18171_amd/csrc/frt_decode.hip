@@ -448,18 +448,18 @@ hipError_t launch_decode_split(const DecodeParams &p, const RopeDev &r, hipStrea
   const int H = p.B * p.Hkv;
   dim3 grid(p.nwaves / kDecWaves + (H + kDecWaves - 1) / kDecWaves);  // + own-token waves
   if (p.D == 128)
-    hipLaunchKernelGGL(decode_split_kernel<128>, grid, dim3(256), 0, s, p, r);
+    dispatch(decode_split_kernel<128>, grid, dim3(256), s, p, r);
   else
-    hipLaunchKernelGGL(decode_split_kernel<64>, grid, dim3(256), 0, s, p, r);
+    dispatch(decode_split_kernel<64>, grid, dim3(256), s, p, r);
   return hipGetLastError();
 }
 
 hipError_t launch_decode_combine(const DecodeParams &p, hipStream_t s) {
   dim3 grid(p.G, p.Hkv, p.B);
   if (p.D == 128)
-    hipLaunchKernelGGL(decode_combine_kernel<128>, grid, dim3(128), 0, s, p);
+    dispatch(decode_combine_kernel<128>, grid, dim3(128), s, p);
   else
-    hipLaunchKernelGGL(decode_combine_kernel<64>, grid, dim3(64), 0, s, p);
+    dispatch(decode_combine_kernel<64>, grid, dim3(64), s, p);
   return hipGetLastError();
 }
 

@@ -487,7 +487,7 @@ hipError_t launch_chunk_attn_fp8(const AttnFp8Params &p, int D, hipStream_t s) {
   dim3 grid((nlog + 7) / 8 * 8);
   dim3 block(kChunkWaves * 64);
   if (D != 128) return hipErrorInvalidValue;  // the host API admits head_dim 128 only
-  hipLaunchKernelGGL((chunk_attn_fp8_kernel<128, kChunkWaves>), grid, block, 0, s, p);
+  dispatch((chunk_attn_fp8_kernel<128, kChunkWaves>), grid, block, s, p);
   return hipGetLastError();
 }
 

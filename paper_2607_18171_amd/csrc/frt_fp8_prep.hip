@@ -161,18 +161,18 @@ __global__ __launch_bounds__(256) void chunk_prep_fp8_kernel(PrepFp8Params p, Ro
 hipError_t launch_rope_append_fp8(const AppendFp8Params &p, const RopeDev &r, hipStream_t s) {
   dim3 grid((p.n + kAppendTokens - 1) / kAppendTokens, p.Hkv, p.B);
   if (p.D == 128)
-    hipLaunchKernelGGL(rope_append_fp8_kernel<128>, grid, dim3(256), 0, s, p, r);
+    dispatch(rope_append_fp8_kernel<128>, grid, dim3(256), s, p, r);
   else
-    hipLaunchKernelGGL(rope_append_fp8_kernel<64>, grid, dim3(256), 0, s, p, r);
+    dispatch(rope_append_fp8_kernel<64>, grid, dim3(256), s, p, r);
   return hipGetLastError();
 }
 
 hipError_t launch_chunk_prep_fp8(const PrepFp8Params &p, const RopeDev &r, hipStream_t s) {
   dim3 grid((p.n_pad + kAppendTokens - 1) / kAppendTokens, p.Hkv, p.B);
   if (p.D == 128)
-    hipLaunchKernelGGL(chunk_prep_fp8_kernel<128>, grid, dim3(256), 0, s, p, r);
+    dispatch(chunk_prep_fp8_kernel<128>, grid, dim3(256), s, p, r);
   else
-    hipLaunchKernelGGL(chunk_prep_fp8_kernel<64>, grid, dim3(256), 0, s, p, r);
+    dispatch(chunk_prep_fp8_kernel<64>, grid, dim3(256), s, p, r);
   return hipGetLastError();
 }
 

@@ -1,6 +1,7 @@
 // Kernel parameter blocks and launchers (internal to libfrt).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -136,6 +137,24 @@ __host__ __device__ inline int decode_piece_waves(int B, int Hkv, int C) {
   return (int)((w + 3) / 4 * 4);
 }
 __host__ __device__ inline size_t decode_split_floats(int G, int D) { return (size_t)G * (2 + D); }
+
+// Timing events for the next kernel dispatch of this host thread. The
+// library's timing sets them; the dispatch then records its own start and end
+// in them (HIP's event-carrying launch), so a timed interval holds the kernel
+// alone and no extra packets go into the stream.
+struct DispatchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+DispatchEvents &pending_dispatch_events();
+
+// Every kernel of the library is launched through this.
+template <typename F, typename... Args>
+void dispatch(F kernel, dim3 grid, dim3 block, hipStream_t s, Args... args) {
+  DispatchEvents &ev = pending_dispatch_events();
+  const hipEvent_t a = ev.start, b = ev.stop;
+  ev = DispatchEvents{};
+  hipExtLaunchKernelGGL(kernel, grid, block, 0u, s, a, b, 0u, args...);
+}
 
 hipError_t launch_rope_append(const AppendParams &p, const RopeDev &r, hipStream_t s);
 hipError_t launch_rope_append_small(const AppendParams &p, const RopeDev &r, hipStream_t s);
