@@ -134,13 +134,15 @@ def _stream(stream) -> Optional[int]:
 V_BLOCK = 32  # slots per V ring block
 
 
-def v_offsets(capacity: int, head_dim: int):
+def v_offsets(capacity: int, head_dim: int, slots=None):
     """Element offset of (slot, dim) inside one head's V ring storage, as an
-    int64 tensor [capacity][head_dim]: blocks of V_BLOCK slots, each stored row
-    by row of the head dimension (a partial last block has rows of
-    capacity % V_BLOCK slots)."""
+    int64 tensor [len(slots)][head_dim] (every slot when None): blocks of
+    V_BLOCK slots, each stored row by row of the head dimension (a partial
+    last block has rows of capacity % V_BLOCK slots)."""
     import torch
-    s = torch.arange(capacity, dtype=torch.int64)[:, None]
+    if slots is None:
+        slots = torch.arange(capacity, dtype=torch.int64)
+    s = torch.as_tensor(slots, dtype=torch.int64).reshape(-1, 1)
     d = torch.arange(head_dim, dtype=torch.int64)[None, :]
     nfull = capacity // V_BLOCK
     w = torch.where(s // V_BLOCK < nfull, V_BLOCK, capacity - V_BLOCK * nfull)
@@ -172,10 +174,7 @@ class Ring:
     def v_index(self, slots=None):
         """Flat element indices into a head's V storage for `slots` (all
         slots when None), shaped [len(slots)][d], on the ring's device."""
-        off = v_offsets(self.C, self.d)
-        if slots is not None:
-            off = off[slots]
-        return off.to(self.v.device)
+        return v_offsets(self.C, self.d, slots).to(self.v.device)
 
     def v_tokens(self):
         """V as bf16 [B][Hkv][C][d] (slot-major copy of the block layout)."""

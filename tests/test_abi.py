@@ -65,6 +65,7 @@ def call_step(r, o, m, n=16, hq=2, ws=FAKE, wsb=1 << 30, out=FAKE, q=FAKE):
 @pytest.mark.parametrize("r,code", [
     (ring(d=96), 3), (ring(d=0), 2), (ring(C=60), 5), (ring(C=0), 2), (ring(k=0), 1),
     (ring(B_=0), 2), (ring(k=FAKE + 2), 5), (ring(s=0), 1),
+    (ring(C=8388608), 2),  # 2^31 bytes of K per head at head_dim 128: one block past the limit
 ])
 def test_append_rejects_bad_ring(r, code):
     assert call_append(r, rope()) == code
