@@ -161,27 +161,75 @@ def cpu_baseline_decode(wl, case, seconds: float):
                       % (wl.B, reps, by / 1e6, dt)}
 
 
-# HBM traffic per launch of the dominant kernel, from rocprofv3 FETCH_SIZE and
-# WRITE_SIZE passes scaled by a plain-copy calibration; used only while the
-# kernel's sources still hash to what the counters were taken on.
 # Default warm-up length: after an idle spell the part needs 15-20 ms of load
 # to reach its steady clock (a 1.3B-like step measured 823 -> 745 -> 727 ->
 # 701 -> 682 -> 672 us in consecutive 5-step windows from a cold start).
 WARMUP_MS = 200
 
+# HBM traffic per launch of the dominant kernel, from rocprofv3 FETCH_SIZE and
+# WRITE_SIZE passes scaled by a plain-copy calibration; used only while the
+# library's machine code for the kernel is the code the counters were taken on.
 TRAFFIC_FILES = {("chunk_attn", "video_1p3b"): "profiles/chunk_attn_video_1p3b.txt",
                  ("decode_split", "decode"): "profiles/decode_split_decode.txt",
                  ("chunk_attn_fp8", "video_1p3b"): "profiles/chunk_attn_fp8_video_1p3b.txt"}
-KERNEL_SOURCES = {"chunk_attn": ["paper_2607_18171_amd/csrc/frt_attn.hip"],
-                  "decode_split": ["paper_2607_18171_amd/csrc/frt_decode.hip"],
-                  "chunk_attn_fp8": ["paper_2607_18171_amd/csrc/frt_fp8_attn.hip",
-                                     "paper_2607_18171_amd/csrc/frt_fp8.hpp"]}
-COMMON_SOURCES = ["paper_2607_18171_amd/csrc/frt_device.hpp",
-                  "paper_2607_18171_amd/csrc/frt_launch.hpp", "paper_2607_18171_amd/build.py"]
+# The kernels' symbols (head_dim 128, the instantiation every bench workload
+# runs) in the library's gfx950 code object.
+KERNEL_SYMBOLS = {"chunk_attn": "17chunk_attn_kernelILi128ELi8E",
+                  "decode_split": "19decode_split_kernelILi128E",
+                  "chunk_attn_fp8": "21chunk_attn_fp8_kernelILi128ELi8E"}
 
 
-def recorded_traffic(kernel: str, workload: str):
+def _elf_symbol_bytes(elf: bytes, part: str):
+    """Name and bytes of every sized symbol whose name contains `part` in an
+    ELF64 image (the kernel's code and its kernel descriptor)."""
+    import struct
+    shoff = struct.unpack_from("<Q", elf, 0x28)[0]
+    shentsize, shnum = struct.unpack_from("<HH", elf, 0x3A)
+    secs = [struct.unpack_from("<IIQQQQIIQQ", elf, shoff + k * shentsize) for k in range(shnum)]
+    out = b""
+    for sec in secs:
+        if sec[1] != 2:  # SHT_SYMTAB
+            continue
+        strtab = secs[sec[6]]
+        for k in range(sec[5] // 24):
+            name_off, _, _, shndx, value, size = struct.unpack_from("<IBBHQQ", elf,
+                                                                    sec[4] + 24 * k)
+            start = strtab[4] + name_off
+            name = elf[start:elf.index(b"\0", start)]
+            if size and part.encode() in name and shndx < shnum:
+                host = secs[shndx]
+                fo = host[4] + (value - host[3])
+                out += name + elf[fo:fo + size]
+    return out or None
+
+
+def kernel_code_sha256(kernel: str, lib_path: str):
+    """sha256 of a kernel's gfx950 machine code and descriptor in the built
+    library (its offload bundles), or None if it is not found."""
     import hashlib
+    import struct
+    data = open(lib_path, "rb").read()
+    magic = b"__CLANG_OFFLOAD_BUNDLE__"
+    pos = data.find(magic)
+    while pos >= 0:
+        n = struct.unpack_from("<Q", data, pos + len(magic))[0]
+        off = pos + len(magic) + 8
+        for _ in range(n):
+            eo, es, tl = struct.unpack_from("<QQQ", data, off)
+            triple = data[off + 24:off + 24 + tl]
+            off += 24 + tl
+            if b"gfx950" in triple and es:
+                code = _elf_symbol_bytes(data[pos + eo:pos + eo + es], KERNEL_SYMBOLS[kernel])
+                if code is not None:
+                    return hashlib.sha256(code).hexdigest()
+        pos = data.find(magic, pos + 1)
+    return None
+
+
+def recorded_traffic(kernel: str, workload: str, lib_path: str):
+    """HBM bytes per launch from the committed profile summary, while the
+    library's machine code for the kernel is the one the counters were taken
+    on; None otherwise."""
     path = TRAFFIC_FILES.get((kernel, workload))
     if path is None or not os.path.exists(os.path.join(ROOT, path)):
         return None
@@ -190,11 +238,8 @@ def recorded_traffic(kernel: str, workload: str):
         if " = " in line:
             k, v = line.split(" = ", 1)
             fields[k.strip()] = v.strip()
-    h = hashlib.sha256()
-    for f in KERNEL_SOURCES[kernel] + COMMON_SOURCES:
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(fh.read())
-    if fields.get("kernel_source_sha256") != h.hexdigest():
+    code = kernel_code_sha256(kernel, lib_path)
+    if code is None or fields.get("kernel_code_sha256") != code:
         return None
     return int(fields["traffic_bytes_per_launch"])
 
@@ -213,7 +258,7 @@ def main(argv=None):
                     help="target length of the oracle's timed CPU sample (0 = skip)")
     ap.add_argument("--fp8", action="store_true",
                     help="the FP8 (e4m3fn) ring and step attention (chunk workloads, head_dim "
-                         "128): frt_stream_attn_step_fp8 then frt_kv_append_fp8")
+                         "128): frt_stream_step_fp8 (attention and the append, fused)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized device buffer 3 times (known HBM traffic for "
                          "scaling FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -285,8 +330,7 @@ def main(argv=None):
         if decode:  # attention and the one-token append in one call
             frt.decode_step(ring, rope, msk, q, kn, vn, out, ws)
         elif args.fp8:
-            frt.stream_attn_step_fp8(ring, rope, msk, q, kn, vn, out, ws)
-            frt.kv_append_fp8(ring, rope, kn, vn)
+            frt.stream_step_fp8(ring, rope, msk, q, kn, vn, out, ws)
         else:
             frt.stream_step(ring, rope, msk, q, kn, vn, out, ws)
 
@@ -361,7 +405,8 @@ def main(argv=None):
         achieved = kbytes_step / (dom["avg_us"] * 1e-6) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": achieved / PEAK_HBM_GBS,
-                "traffic": recorded_traffic("decode_split", wl.name), "kernel": "decode_split"}
+                "traffic": recorded_traffic("decode_split", wl.name, frt.LIB_PATH),
+                "kernel": "decode_split"}
     else:
         value = flops_step / (ms_step * 1e-3) / 1e12
         unit = "TFLOP/s"
@@ -371,7 +416,7 @@ def main(argv=None):
         kname = "chunk_attn_fp8" if args.fp8 else "chunk_attn"
         roof = {"bound": "mfma", "achieved": achieved, "peak": peak,
                 "unit": "TFLOP/s", "frac": achieved / peak,
-                "traffic": recorded_traffic(kname, wl.name), "kernel": kname}
+                "traffic": recorded_traffic(kname, wl.name, frt.LIB_PATH), "kernel": kname}
 
     cpu = None
     if args.cpu_seconds > 0 and not decode:

@@ -280,8 +280,9 @@ frt_status frt_kv_append_fp8(const frt_ring *ring, const frt_fp8_scales *scales,
                              const frt_rope *rope, const void *k_new,
                              const void *v_new, int32_t n_new, void *hip_stream);
 
-/* Workspace bytes frt_stream_attn_step_fp8 needs: query codes and their row
- * scales, the chunk's own key and value codes. */
+/* Workspace bytes frt_stream_attn_step_fp8 and frt_stream_step_fp8 need:
+ * query codes and their row scales, the chunk's own key and value codes, and
+ * each stream's starting position. */
 size_t frt_stream_attn_fp8_workspace_bytes(const frt_ring *ring, int32_t n_new,
                                            int32_t num_q_heads);
 
@@ -303,6 +304,23 @@ frt_status frt_stream_attn_step_fp8(const frt_ring *ring, const frt_fp8_scales *
                                     int32_t num_q_heads, float softmax_scale,
                                     void *workspace, size_t workspace_bytes,
                                     void *out, float *lse, void *hip_stream);
+
+/*
+ * A whole FP8 streaming step: exactly frt_stream_attn_step_fp8 followed by
+ * frt_kv_append_fp8(k_new, v_new, n_new) on the same stream (same outputs,
+ * same ring codes and seq_len afterwards). The append copies the key and
+ * value codes the step has already computed from the workspace into the
+ * ring's slots and advances seq_len in the same launch, after the attention
+ * launch has finished reading the ring. Arguments, workspace and errors as
+ * for frt_stream_attn_step_fp8; n_new <= capacity.
+ */
+frt_status frt_stream_step_fp8(const frt_ring *ring, const frt_fp8_scales *scales,
+                               const frt_rope *rope, const frt_mask *mask,
+                               const void *q, const void *k_new,
+                               const void *v_new, int32_t n_new,
+                               int32_t num_q_heads, float softmax_scale,
+                               void *workspace, size_t workspace_bytes,
+                               void *out, float *lse, void *hip_stream);
 
 /* Static description of a status code. */
 const char *frt_status_str(frt_status status);

@@ -29,7 +29,8 @@ EXPORTS = (
     "frt_stream_attn_workspace_bytes", "frt_stream_attn_step", "frt_stream_step",
     "frt_decode_max_splits",
     "frt_decode_workspace_bytes", "frt_decode_attn", "frt_decode_step", "frt_kv_append_fp8",
-    "frt_stream_attn_fp8_workspace_bytes", "frt_stream_attn_step_fp8", "frt_status_str",
+    "frt_stream_attn_fp8_workspace_bytes", "frt_stream_attn_step_fp8", "frt_stream_step_fp8",
+    "frt_status_str",
     "frt_last_error",
     "frt_timing_enable", "frt_timing_query", "frt_timing_reset",
 )
@@ -99,6 +100,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "frt_stream_attn_fp8_workspace_bytes": (SZ, [RP, I32, I32]),
         "frt_stream_attn_step_fp8": (I32, [RP, SP, OP, MP, P, P, P, I32, I32, ctypes.c_float, P,
                                            SZ, P, P, P]),
+        "frt_stream_step_fp8": (I32, [RP, SP, OP, MP, P, P, P, I32, I32, ctypes.c_float, P,
+                                      SZ, P, P, P]),
         "frt_status_str": (ctypes.c_char_p, [I32]),
         "frt_last_error": (ctypes.c_char_p, []),
         "frt_timing_enable": (I32, [I32]),
@@ -347,6 +350,17 @@ def stream_attn_step_fp8(ring: RingFp8, rope: Rope, msk: CMask, q, k_new, v_new,
     n, hq = q.shape[1], q.shape[2]
     cr, co, cs = ring.c(), rope.c(), ring.scales()
     _check(load_library().frt_stream_attn_step_fp8(
+        ctypes.byref(cr), ctypes.byref(cs), ctypes.byref(co), ctypes.byref(msk), _ptr(q),
+        _ptr(k_new), _ptr(v_new), n, hq, softmax_scale, _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _ptr(out), _ptr(lse), _stream(stream)))
+
+
+def stream_step_fp8(ring: RingFp8, rope: Rope, msk: CMask, q, k_new, v_new, out, workspace,
+                    lse=None, softmax_scale: float = 0.0, stream=None) -> None:
+    """frt_stream_step_fp8: stream_attn_step_fp8 then kv_append_fp8, fused."""
+    n, hq = q.shape[1], q.shape[2]
+    cr, co, cs = ring.c(), rope.c(), ring.scales()
+    _check(load_library().frt_stream_step_fp8(
         ctypes.byref(cr), ctypes.byref(cs), ctypes.byref(co), ctypes.byref(msk), _ptr(q),
         _ptr(k_new), _ptr(v_new), n, hq, softmax_scale, _ptr(workspace),
         workspace.numel() * workspace.element_size(), _ptr(out), _ptr(lse), _stream(stream)))

@@ -421,7 +421,7 @@ frt_status frt_stream_step(const frt_ring *ring, const frt_rope *rope, const frt
 namespace {
 
 struct Fp8Layout {
-  size_t q_off, s_off, k_off, v_off, bytes;
+  size_t q_off, s_off, k_off, v_off, l_off, bytes;
   int n_pad;
 };
 
@@ -434,7 +434,8 @@ Fp8Layout fp8_layout(const frt_ring *r, int n, int hq) {
   L.s_off = round_up(rows * d, 256);
   L.k_off = L.s_off + round_up(rows * 4, 256);
   L.v_off = L.k_off + round_up((size_t)r->num_streams * r->num_kv_heads * L.n_pad * d, 256);
-  L.bytes = L.v_off + round_up((size_t)r->num_streams * r->num_kv_heads * L.n_pad * d, 256);
+  L.l_off = L.v_off + round_up((size_t)r->num_streams * r->num_kv_heads * L.n_pad * d, 256);
+  L.bytes = L.l_off + round_up((size_t)r->num_streams * 8, 256);
   return L;
 }
 
@@ -486,11 +487,18 @@ size_t frt_stream_attn_fp8_workspace_bytes(const frt_ring *ring, int32_t n_new,
   return fp8_layout(ring, n_new, num_q_heads).bytes;
 }
 
-frt_status frt_stream_attn_step_fp8(const frt_ring *ring, const frt_fp8_scales *scales,
-                                    const frt_rope *rope, const frt_mask *mask, const void *q,
-                                    const void *k_new, const void *v_new, int32_t n_new,
-                                    int32_t num_q_heads, float softmax_scale, void *workspace,
-                                    size_t workspace_bytes, void *out, float *lse, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// The FP8 step: preparation and attention, then (append) the chunk's codes
+// into the ring and seq_len advanced, in one launch.
+frt_status stream_fp8_impl(const frt_ring *ring, const frt_fp8_scales *scales,
+                           const frt_rope *rope, const frt_mask *mask, const void *q,
+                           const void *k_new, const void *v_new, int32_t n_new,
+                           int32_t num_q_heads, float softmax_scale, void *workspace,
+                           size_t workspace_bytes, void *out, float *lse, void *stream,
+                           bool append) {
   frt_status s;
   if ((s = check_ring(ring)) != FRT_OK) return s;
   if ((s = check_scales(scales)) != FRT_OK) return s;
@@ -530,6 +538,7 @@ frt_status frt_stream_attn_step_fp8(const frt_ring *ring, const frt_fp8_scales *
   pp.qs = reinterpret_cast<float *>(ws + lay.s_off);
   pp.kr = reinterpret_cast<uint8_t *>(ws + lay.k_off);
   pp.vt = reinterpret_cast<uint8_t *>(ws + lay.v_off);
+  pp.lrec = reinterpret_cast<int64_t *>(ws + lay.l_off);
   pp.sc.k = scales->k_scale;
   pp.sc.v = scales->v_scale;
   pp.B = ring->num_streams;
@@ -568,7 +577,46 @@ frt_status frt_stream_attn_step_fp8(const frt_ring *ring, const frt_fp8_scales *
   hipStream_t st = static_cast<hipStream_t>(stream);
   if ((s = launch("chunk_prep", st, [&] { return launch_chunk_prep_fp8(pp, rd, st); })) != FRT_OK)
     return s;
-  return launch("chunk_attn", st, [&] { return launch_chunk_attn_fp8(ap, ring->head_dim, st); });
+  if ((s = launch("chunk_attn", st, [&] { return launch_chunk_attn_fp8(ap, ring->head_dim, st); })) !=
+      FRT_OK)
+    return s;
+  if (!append) return FRT_OK;
+  ChunkAppendFp8Params cp;
+  cp.kr = pp.kr;
+  cp.vt = pp.vt;
+  cp.lrec = pp.lrec;
+  cp.k_ring = static_cast<uint8_t *>(ring->k_ring);
+  cp.v_ring = static_cast<uint8_t *>(ring->v_ring);
+  cp.seq_len = ring->seq_len;
+  cp.B = pp.B;
+  cp.Hkv = pp.Hkv;
+  cp.D = ring->head_dim;
+  cp.C = ring->capacity;
+  cp.n = n_new;
+  cp.n_pad = lay.n_pad;
+  return launch("chunk_append", st, [&] { return launch_chunk_append_fp8(cp, st); });
+}
+
+}  // namespace
+
+extern "C" {
+
+frt_status frt_stream_attn_step_fp8(const frt_ring *ring, const frt_fp8_scales *scales,
+                                    const frt_rope *rope, const frt_mask *mask, const void *q,
+                                    const void *k_new, const void *v_new, int32_t n_new,
+                                    int32_t num_q_heads, float softmax_scale, void *workspace,
+                                    size_t workspace_bytes, void *out, float *lse, void *stream) {
+  return stream_fp8_impl(ring, scales, rope, mask, q, k_new, v_new, n_new, num_q_heads,
+                         softmax_scale, workspace, workspace_bytes, out, lse, stream, false);
+}
+
+frt_status frt_stream_step_fp8(const frt_ring *ring, const frt_fp8_scales *scales,
+                               const frt_rope *rope, const frt_mask *mask, const void *q,
+                               const void *k_new, const void *v_new, int32_t n_new,
+                               int32_t num_q_heads, float softmax_scale, void *workspace,
+                               size_t workspace_bytes, void *out, float *lse, void *stream) {
+  return stream_fp8_impl(ring, scales, rope, mask, q, k_new, v_new, n_new, num_q_heads,
+                         softmax_scale, workspace, workspace_bytes, out, lse, stream, true);
 }
 
 int32_t frt_decode_max_splits(const frt_ring *ring) {

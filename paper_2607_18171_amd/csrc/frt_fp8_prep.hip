@@ -83,6 +83,7 @@ __global__ __launch_bounds__(256) void chunk_prep_fp8_kernel(PrepFp8Params p, Ro
   const int t0 = tb * kAppendTokens;
   const size_t head = (size_t)b * p.Hkv + kvh;
   const float sk = p.sc.k[head], sv = p.sc.v[head];
+  if (tb == 0 && kvh == 0 && threadIdx.x == 0) p.lrec[b] = L;
 
   // own key codes (as the ring will hold them) and value codes; zero padding
   for (int idx = threadIdx.x; idx < kAppendTokens * CH; idx += 256) {
@@ -156,7 +157,60 @@ __global__ __launch_bounds__(256) void chunk_prep_fp8_kernel(PrepFp8Params p, Ro
   }
 }
 
+// The fused step's append: key rows copied from the codes the preparation
+// pass wrote (kr), value codes re-blocked from its 32-token blocks (vt) at the
+// ring's slots through LDS. seq_len is read by no block of this kernel (L
+// comes from the record the preparation pass left), so one block per stream
+// can advance it.
+template <int D>
+__global__ __launch_bounds__(256) void chunk_append_fp8_kernel(ChunkAppendFp8Params p) {
+  constexpr int CH = D / 16;                // 16-byte chunks per key row
+  constexpr int TS = kAppendTokens + 16;    // LDS row stride (bytes) of the [d][token] tile
+  static_assert(kAppendTokens == 2 * kVBlock, "an append block is two value blocks");
+  __shared__ __attribute__((aligned(16))) uint8_t vs[D * TS];
+  const int tb = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const long long L = p.lrec[b];
+  const int t0 = tb * kAppendTokens;
+  const int ntok = min(kAppendTokens, p.n - t0);
+  const size_t head = (size_t)b * p.Hkv + kvh;
+  const uint8_t *krh = p.kr + head * (size_t)p.n_pad * D;
+  for (int idx = threadIdx.x; idx < kAppendTokens * CH; idx += 256) {
+    const int r = idx / CH, c = idx % CH;
+    if (r >= ntok) continue;
+    const int i = t0 + r;
+    const int slot = (int)((L + i) % p.C);
+    *reinterpret_cast<u32x4 *>(p.k_ring + (head * p.C + slot) * D + c * 16) =
+        *reinterpret_cast<const u32x4 *>(krh + (size_t)i * D + c * 16);
+  }
+  // value codes of tokens t0 .. t0+63: two blocks [d][32] (n_pad is a
+  // multiple of 64, so both lie inside the preparation pass's output)
+  const uint8_t *vth = p.vt + head * (size_t)D * p.n_pad + (size_t)t0 * D;
+  for (int idx = threadIdx.x; idx < 2 * D * 2; idx += 256) {
+    const int kb = idx / (2 * D), d = (idx / 2) % D, h = idx % 2;
+    *reinterpret_cast<u32x4 *>(vs + d * TS + kVBlock * kb + 16 * h) =
+        *reinterpret_cast<const u32x4 *>(vth + (size_t)kb * kVBlock * D + d * kVBlock + 16 * h);
+  }
+  __syncthreads();
+  const int r = threadIdx.x & 63;
+  if (r < ntok) {
+    const int slot = (int)((L + t0 + r) % p.C);
+    uint8_t *vdst = p.v_ring + head * (size_t)D * p.C + vring_elem(slot, 0, p.C, D);
+    const uint32_t w = vring_width(slot, p.C);
+    for (int dd = threadIdx.x >> 6; dd < D; dd += 4) vdst[dd * w] = vs[dd * TS + r];
+  }
+  if (tb == 0 && kvh == 0 && threadIdx.x == 0) p.seq_len[b] = L + p.n;
+}
+
 }  // namespace
+
+hipError_t launch_chunk_append_fp8(const ChunkAppendFp8Params &p, hipStream_t s) {
+  dim3 grid((p.n + kAppendTokens - 1) / kAppendTokens, p.Hkv, p.B);
+  if (p.D == 128)
+    dispatch(chunk_append_fp8_kernel<128>, grid, dim3(256), s, p);
+  else
+    dispatch(chunk_append_fp8_kernel<64>, grid, dim3(256), s, p);
+  return hipGetLastError();
+}
 
 hipError_t launch_rope_append_fp8(const AppendFp8Params &p, const RopeDev &r, hipStream_t s) {
   dim3 grid((p.n + kAppendTokens - 1) / kAppendTokens, p.Hkv, p.B);

@@ -53,9 +53,20 @@ struct PrepFp8Params {
   float *qs;              // [B][Hkv][n*G]     their row scale 2^e
   uint8_t *kr;            // [B][Hkv][n_pad][D] own key codes (as the ring stores them)
   uint8_t *vt;            // [B][Hkv][n_pad*D]  own value codes, ring block layout
+  int64_t *lrec;          // [B]  seq_len at the step's start (for the fused append)
   Fp8Scales sc;
   int B, Hq, Hkv, G, D, n, n_pad;
   double qmul;
+};
+
+// Fused-step append of the FP8 ring from the preparation pass's codes.
+struct ChunkAppendFp8Params {
+  const uint8_t *kr;      // [B][Hkv][n_pad][D] key codes
+  const uint8_t *vt;      // [B][Hkv][n_pad*D] value codes in 32-token blocks [d][32]
+  const int64_t *lrec;    // [B]  seq_len at the step's start
+  uint8_t *k_ring, *v_ring;
+  int64_t *seq_len;
+  int B, Hkv, D, C, n, n_pad;
 };
 
 struct AttnFp8Params {
@@ -165,6 +176,7 @@ hipError_t launch_chunk_append(const ChunkAppendParams &p, hipStream_t s);
 hipError_t launch_rope_append_fp8(const AppendFp8Params &p, const RopeDev &r, hipStream_t s);
 hipError_t launch_chunk_prep_fp8(const PrepFp8Params &p, const RopeDev &r, hipStream_t s);
 hipError_t launch_chunk_attn_fp8(const AttnFp8Params &p, int D, hipStream_t s);
+hipError_t launch_chunk_append_fp8(const ChunkAppendFp8Params &p, hipStream_t s);
 hipError_t launch_decode_split(const DecodeParams &p, const RopeDev &r, hipStream_t s);
 hipError_t launch_decode_combine(const DecodeParams &p, hipStream_t s);
 

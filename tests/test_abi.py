@@ -30,7 +30,7 @@ def declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = frt.load_library()
     names = declared_symbols()
-    assert len(names) == 18
+    assert len(names) == 19
     for name in names:
         assert hasattr(lib, name), name
     assert sorted(B.EXPORTS) == names
@@ -157,3 +157,15 @@ def test_rope_table_fill_matches_oracle_bitwise():
             off += npos * (D // 2) * 2
         assert off == buf.size
         assert lib.frt_rope_table_fill(ctypes.byref(c), buf.ctypes.data, nbytes - 4) == 2
+
+
+def test_kernel_code_hash_finds_the_measured_kernels():
+    """bench.py keys recorded HBM traffic on the dominant kernels' machine code:
+    each must be found in the built library's gfx950 code objects."""
+    import bench
+    lib = frt.binding.LIB_PATH
+    if not os.path.exists(lib):
+        pytest.skip("library not built")
+    hashes = {k: bench.kernel_code_sha256(k, lib) for k in bench.KERNEL_SYMBOLS}
+    assert all(h is not None and len(h) == 64 for h in hashes.values()), hashes
+    assert len(set(hashes.values())) == len(hashes)

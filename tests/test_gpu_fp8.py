@@ -8,7 +8,7 @@ import oracle
 from oracle import fp8
 import paper_2607_18171_amd as frt
 from workloads import (WORKLOADS, RopeSpec, MaskSpec, ROPE_3D, MASK_BLOCK_CAUSAL, MASK_CAUSAL,
-                       make_case, shrink)
+                       make_case, shrink, draw_bf16)
 from gpu_helpers import to_dev, from_dev, bf16_dev_to_f64, gpu_rope, gpu_mask
 
 pytestmark = pytest.mark.gpu
@@ -143,6 +143,44 @@ def test_fp8_attention_full_size_sampled_rows(name):
                                        ks, vs, rows=rows)
     check_fp8(bf16_dev_to_f64(out)[:, rows], ref[:, rows], vmax_fp8(oring, case, vs), name)
     assert np.abs(lse.cpu().numpy()[:, :, rows] - ref_lse[:, :, rows]).max() < 2e-2
+
+
+@pytest.mark.parametrize("name", ["video_small", "video_vpart", "gqa_swa", "mha_causal"])
+def test_fp8_stream_step_equals_attn_then_append(name):
+    """frt_stream_step_fp8 over consecutive steps: the same outputs and lse as
+    frt_stream_attn_step_fp8 + frt_kv_append_fp8, bit for bit, the same ring
+    codes and lengths, and ring codes equal to the FP8 oracle's."""
+    wl = SMALL[name]
+    case = make_case(wl, 4)
+    ks, vs = scales(wl, 4)
+    steps = 3
+    ring, oring, rope = build_fp8_rings(case, ks, vs, extra_tokens=steps * wl.n)
+    twin = frt.RingFp8(wl.B, wl.Hkv, wl.d, wl.C, torch.from_numpy(ks), torch.from_numpy(vs))
+    twin.k.copy_(ring.k)
+    twin.v.copy_(ring.v)
+    twin.seq_len.copy_(ring.seq_len)
+    nbytes = frt.stream_attn_fp8_workspace_bytes(ring, wl.n, wl.Hq)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    ws2 = torch.empty_like(ws)
+    rng = np.random.default_rng(12)
+    for s in range(steps):
+        kn = draw_bf16(rng, case.k_new.shape)  # a fresh chunk each step
+        vn = draw_bf16(rng, case.v_new.shape)
+        q, k, v = to_dev(case.q), to_dev(kn), to_dev(vn)
+        out_a, out_b = torch.empty_like(q), torch.empty_like(q)
+        lse_a = torch.empty((wl.B, wl.Hq, wl.n), dtype=torch.float32, device="cuda")
+        lse_b = torch.empty_like(lse_a)
+        frt.stream_attn_step_fp8(twin, rope, gpu_mask(wl), q, k, v, out_a, ws2, lse=lse_a)
+        frt.kv_append_fp8(twin, rope, k, v)
+        frt.stream_step_fp8(ring, rope, gpu_mask(wl), q, k, v, out_b, ws, lse=lse_b)
+        torch.cuda.synchronize()
+        assert torch.equal(out_a.view(torch.int16), out_b.view(torch.int16)), (name, s)
+        assert torch.equal(lse_a, lse_b), (name, s)
+        assert torch.equal(ring.k, twin.k), (name, s)
+        assert torch.equal(ring.v, twin.v), (name, s)
+        assert torch.equal(ring.seq_len, twin.seq_len), (name, s)
+        fp8.kv_append_fp8(oring, kn, vn, wl.rope, ks, vs)
+    assert ring_codes_equal(ring, oring)
 
 
 def test_fp8_attention_rejects_head_dim_64():
