@@ -57,15 +57,16 @@ def visible_counts(wl, L: int):
     return np.maximum(hi - lo + 1, 0)
 
 
-def step_work(wl, lengths):
-    """(attention flops, minimum HBM bytes) of one step for per-stream lengths."""
+def step_work(wl, lengths, kv_elem_bytes: int = 2):
+    """(attention flops, minimum HBM bytes) of one step for per-stream lengths;
+    ring elements take kv_elem_bytes (2 for bf16, 1 for FP8 codes)."""
     flops = 0
     kv_bytes = 0
     for L in lengths:
         cnt = visible_counts(wl, int(L))
         flops += int(cnt.sum()) * 4 * wl.d * wl.Hq
         # distinct keys read by the stream: union over queries
-        kv_bytes += int(cnt.max()) * wl.Hkv * wl.d * 2 * 2
+        kv_bytes += int(cnt.max()) * wl.Hkv * wl.d * 2 * kv_elem_bytes
     qo_bytes = 2 * wl.B * wl.n * wl.Hq * wl.d * 2
     return flops, kv_bytes + qo_bytes
 
@@ -141,20 +142,32 @@ def cpu_baseline(wl, case, seconds: float, fp8: bool = False):
                       % (len(rows), wl.n, wl.Hq, reps, flops / 1e9, dt)}
 
 
-def cpu_baseline_decode(wl, case, seconds: float):
-    """Time the oracle on the whole decode step, repeated up to about `seconds`."""
+def cpu_baseline_decode(wl, case, seconds: float, fp8: bool = False):
+    """Time the oracle on the whole decode step, repeated up to about `seconds`
+    (with fp8, the FP8 step's oracle on an FP8 ring)."""
     import oracle
-    oring = oracle.new_ring(wl.B, wl.Hkv, wl.C, wl.d)
+    from oracle import fp8 as ofp8
+    if fp8:
+        ks, vs = fp8_scales(wl)
+        oring = ofp8.RingFP8(wl.B, wl.Hkv, wl.C, wl.d)
+    else:
+        oring = oracle.new_ring(wl.B, wl.Hkv, wl.C, wl.d)
     for b in range(wl.B):
         k, v = case.prior_fills[b]
-        oring = oracle.kv_append(oring, k, v, wl.rope, streams=[b])
+        if fp8:
+            ofp8.kv_append_fp8(oring, k, v, wl.rope, ks, vs, streams=[b])
+        else:
+            oring = oracle.kv_append(oring, k, v, wl.rope, streams=[b])
     reps, dt = 0, 0.0
     while reps < 200 and (reps == 0 or dt < seconds):
         t0 = time.perf_counter()
-        oracle.decode_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask)
+        if fp8:
+            ofp8.stream_attn_fp8(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask, ks, vs)
+        else:
+            oracle.decode_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask)
         dt += time.perf_counter() - t0
         reps += 1
-    _, by = step_work(wl, case.prior_lengths)
+    _, by = step_work(wl, case.prior_lengths, 1 if fp8 else 2)
     return {"value": by * reps / dt / 1e9, "unit": "GB/s", "cores": _blas_threads(),
             "kind": "oracle",
             "sample": "whole step, all %d streams, %d repetitions (%.1f MB each, %.1f s)"
@@ -176,7 +189,8 @@ TRAFFIC_FILES = {("chunk_attn", "video_1p3b"): "profiles/chunk_attn_video_1p3b.t
 # runs) in the library's gfx950 code object.
 KERNEL_SYMBOLS = {"chunk_attn": "17chunk_attn_kernelILi128ELi8E",
                   "decode_split": "19decode_split_kernelILi128E",
-                  "chunk_attn_fp8": "21chunk_attn_fp8_kernelILi128ELi8E"}
+                  "chunk_attn_fp8": "21chunk_attn_fp8_kernelILi128ELi8E",
+                  "decode_split_fp8": "23decode_split_fp8_kernelILi128E"}
 
 
 def _elf_symbol_bytes(elf: bytes, part: str):
@@ -257,8 +271,8 @@ def main(argv=None):
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target length of the oracle's timed CPU sample (0 = skip)")
     ap.add_argument("--fp8", action="store_true",
-                    help="the FP8 (e4m3fn) ring and step attention (chunk workloads, head_dim "
-                         "128): frt_stream_step_fp8 (attention and the append, fused)")
+                    help="the FP8 (e4m3fn) ring (head_dim 128): frt_stream_step_fp8, or "
+                         "frt_decode_step_fp8 for the decode workload")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized device buffer 3 times (known HBM traffic for "
                          "scaling FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -282,8 +296,8 @@ def main(argv=None):
     import paper_2607_18171_amd as frt
 
     wl = WORKLOADS[args.workload]
-    if args.fp8 and (wl.n == 1 or wl.d != 128):
-        print("--fp8 covers the chunk workloads with head_dim 128", file=sys.stderr)
+    if args.fp8 and wl.d != 128:
+        print("--fp8 covers the workloads with head_dim 128", file=sys.stderr)
         return 2
     case = make_case(wl, args.seed)
     dev = torch.device("cuda", 0)
@@ -316,7 +330,10 @@ def main(argv=None):
     out = torch.empty_like(q)
     msk = frt.mask(wl.mask.kind, wl.mask.block, wl.mask.window)
     decode = wl.n == 1
-    if decode:
+    if decode and args.fp8:
+        ws = torch.empty(frt.decode_fp8_workspace_bytes(ring, wl.Hq), dtype=torch.uint8,
+                         device=dev)
+    elif decode:
         ws = torch.empty(frt.decode_workspace_bytes(ring, wl.Hq), dtype=torch.uint8, device=dev)
     elif args.fp8:
         ws = torch.empty(frt.stream_attn_fp8_workspace_bytes(ring, wl.n, wl.Hq),
@@ -327,7 +344,9 @@ def main(argv=None):
     torch.cuda.synchronize()
 
     def step():
-        if decode:  # attention and the one-token append in one call
+        if decode and args.fp8:
+            frt.decode_step_fp8(ring, rope, msk, q, kn, vn, out, ws)
+        elif decode:  # attention and the one-token append in one call
             frt.decode_step(ring, rope, msk, q, kn, vn, out, ws)
         elif args.fp8:
             frt.stream_step_fp8(ring, rope, msk, q, kn, vn, out, ws)
@@ -345,7 +364,9 @@ def main(argv=None):
         # attention alone and the stream lengths stay those of the workload;
         # the chunk steps see a window of the ring that is already full.
         def warm():
-            if decode:
+            if decode and args.fp8:
+                frt.decode_attn_fp8(ring, rope, msk, q, kn, vn, out, ws)
+            elif decode:
                 frt.decode_attn(ring, rope, msk, q, kn, vn, out, ws)
             else:
                 step()
@@ -377,7 +398,7 @@ def main(argv=None):
         # algorithmic work (lengths advance by n per step)
         flops = bytes_ = 0
         for s in range(args.steps):
-            f, by = step_work(wl, lengths + s * wl.n)
+            f, by = step_work(wl, lengths + s * wl.n, 1 if args.fp8 else 2)
             flops += f
             bytes_ += by
         return ev0.elapsed_time(ev1) / args.steps, flops / args.steps, bytes_ / args.steps
@@ -403,10 +424,10 @@ def main(argv=None):
         unit = "GB/s"
         dom = kernels["decode_split"]
         achieved = kbytes_step / (dom["avg_us"] * 1e-6) / 1e9
+        kname = "decode_split_fp8" if args.fp8 else "decode_split"
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": achieved / PEAK_HBM_GBS,
-                "traffic": recorded_traffic("decode_split", wl.name, frt.LIB_PATH),
-                "kernel": "decode_split"}
+                "traffic": recorded_traffic(kname, wl.name, frt.LIB_PATH), "kernel": kname}
     else:
         value = flops_step / (ms_step * 1e-3) / 1e12
         unit = "TFLOP/s"
@@ -422,7 +443,7 @@ def main(argv=None):
     if args.cpu_seconds > 0 and not decode:
         cpu = cpu_baseline(wl, case, args.cpu_seconds, fp8=args.fp8)
     elif args.cpu_seconds > 0:
-        cpu = cpu_baseline_decode(wl, case, args.cpu_seconds)
+        cpu = cpu_baseline_decode(wl, case, args.cpu_seconds, fp8=args.fp8)
 
     line = {
         "metric": METRIC, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps,

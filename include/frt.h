@@ -322,6 +322,42 @@ frt_status frt_stream_step_fp8(const frt_ring *ring, const frt_fp8_scales *scale
                                void *workspace, size_t workspace_bytes,
                                void *out, float *lse, void *hip_stream);
 
+/* Workspace bytes frt_decode_attn_fp8 and frt_decode_step_fp8 need: one
+ * partial per KV piece and one per (stream, KV head) for the step's own
+ * token, which also carries the token's key and value codes. */
+size_t frt_decode_fp8_workspace_bytes(const frt_ring *ring, int32_t num_q_heads);
+
+/*
+ * frt_decode_attn over an FP8 ring (head_dim 128): one token per stream,
+ * the same arithmetic as frt_stream_attn_step_fp8 with n_new = 1 (query
+ * codes with a power-of-two scale per query, FP8 contractions with fp32
+ * accumulation, coded weights p = code(2^(s - m + 7))). The ring is cut
+ * into KV pieces as in frt_decode_attn; each piece codes its weights against
+ * its own integer reference max, and the pieces' partials are merged with
+ * power-of-two rescaling. The step's own key and value are coded as
+ * frt_kv_append_fp8 stores them. Tensors, checks and errors as
+ * frt_decode_attn, plus FRT_ERR_UNSUPPORTED for head_dim != 128.
+ */
+frt_status frt_decode_attn_fp8(const frt_ring *ring, const frt_fp8_scales *scales,
+                               const frt_rope *rope, const frt_mask *mask,
+                               const void *q, const void *k_new, const void *v_new,
+                               int32_t num_q_heads, float softmax_scale,
+                               void *workspace, size_t workspace_bytes,
+                               void *out, float *lse, void *hip_stream);
+
+/*
+ * A whole FP8 decode step: exactly frt_decode_attn_fp8 followed by
+ * frt_kv_append_fp8(k_new, v_new, 1) on the same stream (same outputs, same
+ * ring codes and seq_len afterwards). The combine pass stores the token's
+ * key and value codes, which the split pass computed, and advances seq_len.
+ */
+frt_status frt_decode_step_fp8(const frt_ring *ring, const frt_fp8_scales *scales,
+                               const frt_rope *rope, const frt_mask *mask,
+                               const void *q, const void *k_new, const void *v_new,
+                               int32_t num_q_heads, float softmax_scale,
+                               void *workspace, size_t workspace_bytes,
+                               void *out, float *lse, void *hip_stream);
+
 /* Static description of a status code. */
 const char *frt_status_str(frt_status status);
 

@@ -30,6 +30,7 @@ EXPORTS = (
     "frt_decode_max_splits",
     "frt_decode_workspace_bytes", "frt_decode_attn", "frt_decode_step", "frt_kv_append_fp8",
     "frt_stream_attn_fp8_workspace_bytes", "frt_stream_attn_step_fp8", "frt_stream_step_fp8",
+    "frt_decode_fp8_workspace_bytes", "frt_decode_attn_fp8", "frt_decode_step_fp8",
     "frt_status_str",
     "frt_last_error",
     "frt_timing_enable", "frt_timing_query", "frt_timing_reset",
@@ -102,6 +103,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                            SZ, P, P, P]),
         "frt_stream_step_fp8": (I32, [RP, SP, OP, MP, P, P, P, I32, I32, ctypes.c_float, P,
                                       SZ, P, P, P]),
+        "frt_decode_fp8_workspace_bytes": (SZ, [RP, I32]),
+        "frt_decode_attn_fp8": (I32, [RP, SP, OP, MP, P, P, P, I32, ctypes.c_float, P, SZ, P, P,
+                                      P]),
+        "frt_decode_step_fp8": (I32, [RP, SP, OP, MP, P, P, P, I32, ctypes.c_float, P, SZ, P, P,
+                                      P]),
         "frt_status_str": (ctypes.c_char_p, [I32]),
         "frt_last_error": (ctypes.c_char_p, []),
         "frt_timing_enable": (I32, [I32]),
@@ -364,6 +370,35 @@ def stream_step_fp8(ring: RingFp8, rope: Rope, msk: CMask, q, k_new, v_new, out,
         ctypes.byref(cr), ctypes.byref(cs), ctypes.byref(co), ctypes.byref(msk), _ptr(q),
         _ptr(k_new), _ptr(v_new), n, hq, softmax_scale, _ptr(workspace),
         workspace.numel() * workspace.element_size(), _ptr(out), _ptr(lse), _stream(stream)))
+
+
+def decode_fp8_workspace_bytes(ring: RingFp8, num_q_heads: int) -> int:
+    cr = ring.c()
+    return int(load_library().frt_decode_fp8_workspace_bytes(ctypes.byref(cr), num_q_heads))
+
+
+def _decode_fp8(fn, ring, rope, msk, q, k_new, v_new, out, workspace, lse, softmax_scale,
+                stream):
+    hq = q.shape[2]
+    cr, co, cs = ring.c(), rope.c(), ring.scales()
+    _check(fn(ctypes.byref(cr), ctypes.byref(cs), ctypes.byref(co), ctypes.byref(msk), _ptr(q),
+              _ptr(k_new), _ptr(v_new), hq, softmax_scale, _ptr(workspace),
+              workspace.numel() * workspace.element_size(), _ptr(out), _ptr(lse),
+              _stream(stream)))
+
+
+def decode_attn_fp8(ring: RingFp8, rope: Rope, msk: CMask, q, k_new, v_new, out, workspace,
+                    lse=None, softmax_scale: float = 0.0, stream=None) -> None:
+    """frt_decode_attn_fp8: q/out bf16 [B][1][Hq][d], k_new/v_new bf16 [B][1][Hkv][d]."""
+    _decode_fp8(load_library().frt_decode_attn_fp8, ring, rope, msk, q, k_new, v_new, out,
+                workspace, lse, softmax_scale, stream)
+
+
+def decode_step_fp8(ring: RingFp8, rope: Rope, msk: CMask, q, k_new, v_new, out, workspace,
+                    lse=None, softmax_scale: float = 0.0, stream=None) -> None:
+    """frt_decode_step_fp8: decode_attn_fp8 then the one-token kv_append_fp8, fused."""
+    _decode_fp8(load_library().frt_decode_step_fp8, ring, rope, msk, q, k_new, v_new, out,
+                workspace, lse, softmax_scale, stream)
 
 
 def timing_enable(on: bool = True) -> None:

@@ -610,6 +610,102 @@ frt_status frt_stream_attn_step_fp8(const frt_ring *ring, const frt_fp8_scales *
                          softmax_scale, workspace, workspace_bytes, out, lse, stream, false);
 }
 
+size_t frt_decode_fp8_workspace_bytes(const frt_ring *ring, int32_t num_q_heads) {
+  if (!ring || ring->num_kv_heads <= 0 || num_q_heads <= 0 || ring->head_dim <= 0) return 0;
+  const int G = num_q_heads / ring->num_kv_heads;
+  // a partial per piece wave, and one per (stream, KV head) for its own token
+  const size_t heads = (size_t)ring->num_streams * ring->num_kv_heads;
+  return ((size_t)frt_decode_max_splits(ring) + heads) *
+         decode_fp8_split_floats(G, ring->head_dim) * sizeof(float);
+}
+
+}  // extern "C"
+
+namespace {
+
+frt_status decode_fp8_impl(const frt_ring *ring, const frt_fp8_scales *scales,
+                           const frt_rope *rope, const frt_mask *mask, const void *q,
+                           const void *k_new, const void *v_new, int32_t num_q_heads,
+                           float softmax_scale, void *workspace, size_t workspace_bytes,
+                           void *out, float *lse, void *stream, bool append) {
+  frt_status s;
+  if ((s = check_ring(ring)) != FRT_OK) return s;
+  if ((s = check_scales(scales)) != FRT_OK) return s;
+  if (ring->head_dim != 128)
+    return fail(FRT_ERR_UNSUPPORTED, "FP8 decode supports head_dim 128 (got %d)",
+                ring->head_dim);
+  if ((s = check_rope(rope, ring->head_dim)) != FRT_OK) return s;
+  if ((s = check_mask(mask, ring->capacity)) != FRT_OK) return s;
+  if (num_q_heads < 1 || num_q_heads % ring->num_kv_heads)
+    return fail(FRT_ERR_SHAPE, "num_q_heads=%d is not a multiple of num_kv_heads=%d", num_q_heads,
+                ring->num_kv_heads);
+  const int G = num_q_heads / ring->num_kv_heads;
+  if (G > 16) return fail(FRT_ERR_UNSUPPORTED, "decode supports up to 16 query heads per KV head");
+  if ((s = check_io(q, "q")) != FRT_OK) return s;
+  if ((s = check_io(k_new, "k_new")) != FRT_OK) return s;
+  if ((s = check_io(v_new, "v_new")) != FRT_OK) return s;
+  if ((s = check_io(out, "out")) != FRT_OK) return s;
+  if (lse && !aligned(lse, 4)) return fail(FRT_ERR_ALIGN, "lse must be 4-byte aligned");
+  const size_t need = frt_decode_fp8_workspace_bytes(ring, num_q_heads);
+  if (!workspace) return fail(FRT_ERR_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (workspace_bytes < need)
+    return fail(FRT_ERR_WORKSPACE, "workspace %zu < %zu bytes", workspace_bytes, need);
+  if (!aligned(workspace, 16)) return fail(FRT_ERR_ALIGN, "workspace must be 16-byte aligned");
+
+  DecodeFp8Params p;
+  p.q = static_cast<const uint16_t *>(q);
+  p.k_new = static_cast<const uint16_t *>(k_new);
+  p.v_new = static_cast<const uint16_t *>(v_new);
+  p.k_ring = static_cast<uint8_t *>(ring->k_ring);
+  p.v_ring = static_cast<uint8_t *>(ring->v_ring);
+  p.seq_len = ring->seq_len;
+  p.sc.k = scales->k_scale;
+  p.sc.v = scales->v_scale;
+  p.ws = static_cast<float *>(workspace);
+  p.out = static_cast<uint16_t *>(out);
+  p.lse = lse;
+  p.B = ring->num_streams;
+  p.Hq = num_q_heads;
+  p.Hkv = ring->num_kv_heads;
+  p.G = G;
+  p.D = ring->head_dim;
+  p.C = ring->capacity;
+  p.nwaves = frt_decode_max_splits(ring);
+  p.mask_kind = mask->kind;
+  p.mask_block = mask->block;
+  p.mask_window = mask->window;
+  p.append = append ? 1 : 0;
+  p.qmul = q_multiplier(softmax_scale, ring->head_dim);
+  const RopeDev rd = rope_dev(rope);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if ((s = launch("decode_split", st, [&] { return launch_decode_split_fp8(p, rd, st); })) !=
+      FRT_OK)
+    return s;
+  return launch("decode_combine", st, [&] { return launch_decode_combine_fp8(p, st); });
+}
+
+}  // namespace
+
+extern "C" {
+
+frt_status frt_decode_attn_fp8(const frt_ring *ring, const frt_fp8_scales *scales,
+                               const frt_rope *rope, const frt_mask *mask, const void *q,
+                               const void *k_new, const void *v_new, int32_t num_q_heads,
+                               float softmax_scale, void *workspace, size_t workspace_bytes,
+                               void *out, float *lse, void *stream) {
+  return decode_fp8_impl(ring, scales, rope, mask, q, k_new, v_new, num_q_heads, softmax_scale,
+                         workspace, workspace_bytes, out, lse, stream, false);
+}
+
+frt_status frt_decode_step_fp8(const frt_ring *ring, const frt_fp8_scales *scales,
+                               const frt_rope *rope, const frt_mask *mask, const void *q,
+                               const void *k_new, const void *v_new, int32_t num_q_heads,
+                               float softmax_scale, void *workspace, size_t workspace_bytes,
+                               void *out, float *lse, void *stream) {
+  return decode_fp8_impl(ring, scales, rope, mask, q, k_new, v_new, num_q_heads, softmax_scale,
+                         workspace, workspace_bytes, out, lse, stream, true);
+}
+
 frt_status frt_stream_step_fp8(const frt_ring *ring, const frt_fp8_scales *scales,
                                const frt_rope *rope, const frt_mask *mask, const void *q,
                                const void *k_new, const void *v_new, int32_t n_new,

@@ -41,4 +41,30 @@ __device__ __forceinline__ uint32_t e4m3x4_inrange(float a, float b, float c, fl
   return __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
 }
 
+// Codes of the 8 values v[0..7] / s (float division, nearest even).
+__device__ __forceinline__ u32x2 code8(const float v[8], float s) {
+  u32x2 w;
+  w[0] = e4m3x4(__fdiv_rn(v[0], s), __fdiv_rn(v[1], s), __fdiv_rn(v[2], s), __fdiv_rn(v[3], s));
+  w[1] = e4m3x4(__fdiv_rn(v[4], s), __fdiv_rn(v[5], s), __fdiv_rn(v[6], s), __fdiv_rn(v[7], s));
+  return w;
+}
+
+__device__ __forceinline__ void bf16x8_to_f32(u32x4 x, float v[8]) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    v[2 * w] = bf16_bits_to_f32(x[w] & 0xFFFFu);
+    v[2 * w + 1] = bf16_bits_to_f32(x[w] >> 16);
+  }
+}
+
+// The power-of-two row scale of a query: the smallest e with mx <= 448 * 2^e
+// (mx = max |a| over the row; 0 gives 0). mx = f * 2^k with f in [1, 2) and
+// 448 = 1.75 * 2^8.
+__device__ __forceinline__ int fp8_row_exponent(float mx) {
+  if (!(mx > 0.f)) return 0;
+  const uint32_t bits = __float_as_uint(mx);
+  return (int)(bits >> 23) - 127 - 8 + ((bits & 0x7FFFFFu) > 0x600000u ? 1 : 0);
+}
+
+
 }  // namespace frt

@@ -14,22 +14,6 @@ namespace frt {
 
 namespace {
 
-// Codes of the 8 values v[0..7] / s (float division, nearest even).
-__device__ __forceinline__ u32x2 code8(const float v[8], float s) {
-  u32x2 w;
-  w[0] = e4m3x4(__fdiv_rn(v[0], s), __fdiv_rn(v[1], s), __fdiv_rn(v[2], s), __fdiv_rn(v[3], s));
-  w[1] = e4m3x4(__fdiv_rn(v[4], s), __fdiv_rn(v[5], s), __fdiv_rn(v[6], s), __fdiv_rn(v[7], s));
-  return w;
-}
-
-__device__ __forceinline__ void bf16x8_to_f32(u32x4 x, float v[8]) {
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    v[2 * w] = bf16_bits_to_f32(x[w] & 0xFFFFu);
-    v[2 * w + 1] = bf16_bits_to_f32(x[w] >> 16);
-  }
-}
-
 // One block per 64 tokens of one (stream, KV head); the value codes go
 // through LDS so that the block layout is written token-contiguous.
 template <int D>
@@ -124,12 +108,7 @@ __global__ __launch_bounds__(256) void chunk_prep_fp8_kernel(PrepFp8Params p, Ro
     for (int j = 0; j < 8; ++j) mx = fmaxf(mx, fabsf(a[j]));
 #pragma unroll
     for (int off = 1; off < CH; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
-    // smallest e with mx <= 448 * 2^e: mx = f * 2^k, f in [1, 2); 448 = 1.75 * 2^8
-    int e = 0;
-    if (mx > 0.f) {
-      const uint32_t bits = __float_as_uint(mx);
-      e = (int)(bits >> 23) - 127 - 8 + ((bits & 0x7FFFFFu) > 0x600000u ? 1 : 0);
-    }
+    const int e = fp8_row_exponent(mx);
     float sa[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) sa[j] = ldexpf(a[j], -e);

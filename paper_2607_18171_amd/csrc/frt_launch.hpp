@@ -122,6 +122,24 @@ struct DecodeParams {
   double qmul;
 };
 
+// One-token decode over an FP8 ring (head_dim 128).
+struct DecodeFp8Params {
+  const uint16_t *q;       // [B][1][Hq][D] bf16
+  const uint16_t *k_new;   // [B][1][Hkv][D] bf16
+  const uint16_t *v_new;   // [B][1][Hkv][D] bf16
+  uint8_t *k_ring, *v_ring;  // written only by the combine pass, and only with append
+  int64_t *seq_len;
+  Fp8Scales sc;
+  float *ws;               // partials: nwaves + B * Hkv
+  uint16_t *out;           // [B][1][Hq][D]
+  float *lse;              // [B][Hq][1] or null
+  int B, Hq, Hkv, G, D, C;
+  int nwaves;              // piece waves of the split pass (multiple of 4)
+  int mask_kind, mask_block, mask_window;
+  int append;              // combine pass also appends the token to the ring
+  double qmul;
+};
+
 constexpr int kAppendTokens = 64;   // tokens per append / prep block
 constexpr int kAppendSmall = 16;    // appends up to this many tokens take one launch
 constexpr int kChunkBN = 64;        // keys per attention tile
@@ -148,6 +166,11 @@ __host__ __device__ inline int decode_piece_waves(int B, int Hkv, int C) {
   return (int)((w + 3) / 4 * 4);
 }
 __host__ __device__ inline size_t decode_split_floats(int G, int D) { return (size_t)G * (2 + D); }
+// Floats of one FP8 decode partial: max[G], sum[G], out[G][D], then (in a
+// head's own-token slot) 4 header words and the token's key and value codes.
+__host__ __device__ inline size_t decode_fp8_split_floats(int G, int D) {
+  return ((size_t)G * (2 + D) + 4 + (size_t)D / 2 + 3) / 4 * 4;
+}
 
 // Timing events for the next kernel dispatch of this host thread. The
 // library's timing sets them; the dispatch then records its own start and end
@@ -177,6 +200,8 @@ hipError_t launch_rope_append_fp8(const AppendFp8Params &p, const RopeDev &r, hi
 hipError_t launch_chunk_prep_fp8(const PrepFp8Params &p, const RopeDev &r, hipStream_t s);
 hipError_t launch_chunk_attn_fp8(const AttnFp8Params &p, int D, hipStream_t s);
 hipError_t launch_chunk_append_fp8(const ChunkAppendFp8Params &p, hipStream_t s);
+hipError_t launch_decode_split_fp8(const DecodeFp8Params &p, const RopeDev &r, hipStream_t s);
+hipError_t launch_decode_combine_fp8(const DecodeFp8Params &p, hipStream_t s);
 hipError_t launch_decode_split(const DecodeParams &p, const RopeDev &r, hipStream_t s);
 hipError_t launch_decode_combine(const DecodeParams &p, hipStream_t s);
 

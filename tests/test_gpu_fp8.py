@@ -192,3 +192,100 @@ def test_fp8_attention_rejects_head_dim_64():
     assert ring_codes_equal(ring, oring)  # the append supports head_dim 64
     with pytest.raises(frt.FrtError):
         run_fp8_step(case, ring, rope)
+
+
+# ---- FP8 decode: the FP8 step's attention with one token per stream ----
+
+DECODE = {
+    "decode": (WORKLOADS["decode"], None),
+    "split_edges": (shrink(WORKLOADS["decode"], B=6, C=1024), [0, 1, 255, 256, 257, 1023]),
+    "wrapped_window": (shrink(WORKLOADS["decode"], B=3, Hq=8, Hkv=1, C=512,
+                              mask=MaskSpec(MASK_CAUSAL, 0, 300)), [1000, 299, 512]),
+    "mha_g1": (shrink(WORKLOADS["decode"], B=2, Hq=4, Hkv=4, C=264), [100, 263]),
+    "g16": (shrink(WORKLOADS["decode"], B=2, Hq=32, Hkv=2, C=328), [327, 40]),
+    "block_causal": (shrink(WORKLOADS["decode"], B=2, Hq=8, Hkv=2, C=512,
+                            mask=MaskSpec(MASK_BLOCK_CAUSAL, 128, 2)), [300, 511]),
+}
+
+
+def decode_case(name, seed):
+    wl, lengths = DECODE[name]
+    case = make_case(wl, seed, lengths=None if lengths is None else np.array(lengths))
+    ks, vs = scales(wl, seed)
+    return wl, case, ks, vs
+
+
+def run_decode_fp8(wl, case, ring, rope, step=False):
+    q, k, v = to_dev(case.q), to_dev(case.k_new), to_dev(case.v_new)
+    out = torch.empty_like(q)
+    lse = torch.empty((wl.B, wl.Hq, 1), dtype=torch.float32, device="cuda")
+    ws = torch.empty(frt.decode_fp8_workspace_bytes(ring, wl.Hq), dtype=torch.uint8,
+                     device="cuda")
+    fn = frt.decode_step_fp8 if step else frt.decode_attn_fp8
+    fn(ring, rope, gpu_mask(wl), q, k, v, out, ws, lse=lse)
+    torch.cuda.synchronize()
+    return out, lse
+
+
+@pytest.mark.parametrize("name", sorted(DECODE))
+def test_fp8_decode_matches_oracle(name):
+    wl, case, ks, vs = decode_case(name, 0)
+    ring, oring, rope = build_fp8_rings(case, ks, vs)
+    out, lse = run_decode_fp8(wl, case, ring, rope)
+    ref, ref_lse = fp8.stream_attn_fp8(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask,
+                                       ks, vs)
+    check_fp8(bf16_dev_to_f64(out), ref, vmax_fp8(oring, case, vs), name)
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() < 2e-2
+    assert ring_codes_equal(ring, oring)  # decode attention reads the ring only
+
+
+@pytest.mark.parametrize("name", ["split_edges", "wrapped_window", "g16"])
+def test_fp8_decode_step_equals_attn_then_append(name):
+    """frt_decode_step_fp8 over consecutive steps: the same outputs and lse as
+    frt_decode_attn_fp8 + frt_kv_append_fp8, bit for bit, the same ring codes
+    and lengths, and ring codes equal to the FP8 oracle's."""
+    wl, case, ks, vs = decode_case(name, 3)
+    steps = 3
+    ring, oring, rope = build_fp8_rings(case, ks, vs, extra_tokens=steps)
+    twin = frt.RingFp8(wl.B, wl.Hkv, wl.d, wl.C, torch.from_numpy(ks), torch.from_numpy(vs))
+    twin.k.copy_(ring.k)
+    twin.v.copy_(ring.v)
+    twin.seq_len.copy_(ring.seq_len)
+    nbytes = frt.decode_fp8_workspace_bytes(ring, wl.Hq)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    ws2 = torch.empty_like(ws)
+    rng = np.random.default_rng(13)
+    for s in range(steps):
+        qn = draw_bf16(rng, case.q.shape)
+        kn = draw_bf16(rng, case.k_new.shape)
+        vn = draw_bf16(rng, case.v_new.shape)
+        q, k, v = to_dev(qn), to_dev(kn), to_dev(vn)
+        out_a, out_b = torch.empty_like(q), torch.empty_like(q)
+        lse_a = torch.empty((wl.B, wl.Hq, 1), dtype=torch.float32, device="cuda")
+        lse_b = torch.empty_like(lse_a)
+        frt.decode_attn_fp8(twin, rope, gpu_mask(wl), q, k, v, out_a, ws2, lse=lse_a)
+        frt.kv_append_fp8(twin, rope, k, v)
+        frt.decode_step_fp8(ring, rope, gpu_mask(wl), q, k, v, out_b, ws, lse=lse_b)
+        torch.cuda.synchronize()
+        assert torch.equal(out_a.view(torch.int16), out_b.view(torch.int16)), (name, s)
+        assert torch.equal(lse_a, lse_b), (name, s)
+        assert torch.equal(ring.k, twin.k), (name, s)
+        assert torch.equal(ring.v, twin.v), (name, s)
+        assert torch.equal(ring.seq_len, twin.seq_len), (name, s)
+        ref, _ = fp8.stream_attn_fp8(oring, qn, kn, vn, wl.rope, wl.mask, ks, vs)
+        vmax = max(vmax_fp8(oring, case, vs),
+                   max(np.abs(fp8.e4m3_decode(fp8.stored_v8(vn[b, :, h, :], vs[b, h])) * vs[b, h]).max()
+                       for b in range(wl.B) for h in range(wl.Hkv)))
+        check_fp8(bf16_dev_to_f64(out_b), ref, vmax, "%s step %d" % (name, s))
+        fp8.kv_append_fp8(oring, kn, vn, wl.rope, ks, vs)
+    assert ring_codes_equal(ring, oring)
+
+
+def test_fp8_decode_rejects_head_dim_64():
+    wl = shrink(WORKLOADS["decode"], B=1, Hq=2, Hkv=1, d=64, C=64,
+                rope=RopeSpec(0), mask=MaskSpec(MASK_CAUSAL, 0, 0))
+    case = make_case(wl, 0, lengths=np.array([10]))
+    ks, vs = scales(wl, 0)
+    ring, oring, rope = build_fp8_rings(case, ks, vs)
+    with pytest.raises(frt.FrtError):
+        run_decode_fp8(wl, case, ring, rope)
