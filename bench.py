@@ -184,7 +184,8 @@ WARMUP_MS = 200
 # library's machine code for the kernel is the code the counters were taken on.
 TRAFFIC_FILES = {("chunk_attn", "video_1p3b"): "profiles/chunk_attn_video_1p3b.txt",
                  ("decode_split", "decode"): "profiles/decode_split_decode.txt",
-                 ("chunk_attn_fp8", "video_1p3b"): "profiles/chunk_attn_fp8_video_1p3b.txt"}
+                 ("chunk_attn_fp8", "video_1p3b"): "profiles/chunk_attn_fp8_video_1p3b.txt",
+                 ("decode_split_fp8", "decode"): "profiles/decode_split_fp8_decode.txt"}
 # The kernels' symbols (head_dim 128, the instantiation every bench workload
 # runs) in the library's gfx950 code object.
 KERNEL_SYMBOLS = {"chunk_attn": "17chunk_attn_kernelILi128ELi8E",
