@@ -175,8 +175,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecWavesPe
     const int rlo = (int)(rlo64 < -0x40000000LL ? -0x40000000LL : rlo64);
     const int rhi = (int)(rhi64 > 0x40000000LL ? 0x40000000LL : rhi64);
 
-    // the query's loads go first: vector loads retire in order
-    query_frag(b, kvh, st.L, qf);
 
     // tile i of the piece: K rows (block kb, A-row rho = c16 -> token
     // 8*(rho/4) + 4*kb + rho%4 of the tile) and V rows (d = 16*db + c16,
@@ -212,6 +210,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecWavesPe
 #pragma unroll
     for (int j = 0; j < kDecBufs; ++j)
       if (j < cnt) issue(j, j);
+    // The query is loaded and rotated while the first tiles are in flight:
+    // waiting for its loads waits for theirs too (loads retire in order),
+    // but the wave's streaming starts a round trip and the rotation earlier.
+    query_frag(b, kvh, st.L, qf);
 #pragma unroll
     for (int i = 0; i < kDecChunk; ++i) {
       const int buf = i % kDecBufs;
