@@ -72,6 +72,9 @@ SMALL = {
                       mask=MaskSpec(MASK_CAUSAL, 0, 200), len_lo=0, len_hi=800),
     "mha_causal": shrink(WORKLOADS["prefill_swa"], B=2, Hq=4, Hkv=4, n=37, C=512,
                          mask=MaskSpec(MASK_CAUSAL, 0, 0), len_lo=0, len_hi=400),
+    "rope_none": shrink(WORKLOADS["prefill_swa"], B=2, Hq=2, Hkv=1, n=33, C=64,
+                        rope=RopeSpec(0), mask=MaskSpec(MASK_CAUSAL, 0, 50),
+                        len_lo=0, len_hi=300),
 }
 
 # Error sources between the kernel and the FP8 oracle: fp32 accumulation of
@@ -181,6 +184,25 @@ def test_fp8_stream_step_equals_attn_then_append(name):
         assert torch.equal(ring.seq_len, twin.seq_len), (name, s)
         fp8.kv_append_fp8(oring, kn, vn, wl.rope, ks, vs)
     assert ring_codes_equal(ring, oring)
+
+
+def test_fp8_saturating_scales():
+    """Scales small enough that many values lie beyond +-448 codes: the ring
+    holds the clamped codes bit for bit as the oracle does, and attention
+    over them (and the step's own clamped codes) stays within tolerance."""
+    wl = SMALL["gqa_swa"]
+    case = make_case(wl, 5)
+    ks = np.full((wl.B, wl.Hkv), 2e-3, np.float32)  # |k| > 0.9 saturates
+    vs = np.full((wl.B, wl.Hkv), 3e-3, np.float32)
+    ring, oring, rope = build_fp8_rings(case, ks, vs)
+    codes = ring.k.cpu().numpy()
+    assert np.isin(codes, [0x7e, 0xfe]).mean() > 0.1  # the clamp is exercised
+    assert ring_codes_equal(ring, oring)
+    out, lse = run_fp8_step(case, ring, rope)
+    ref, ref_lse = fp8.stream_attn_fp8(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask,
+                                       ks, vs)
+    check_fp8(bf16_dev_to_f64(out), ref, vmax_fp8(oring, case, vs), "saturating")
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() < 2e-2
 
 
 def test_fp8_attention_rejects_head_dim_64():
