@@ -289,8 +289,8 @@ def main(argv=None):
         return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the chunk step runs on one MI355X and nothing "
-              "crosses GPUs in this build (requested --gpus %d)" % args.gpus, file=sys.stderr)
+        print("bench.py measures one GPU only: the step runs on one MI355X and nothing in this "
+              "library crosses GPUs (requested --gpus %d)" % args.gpus, file=sys.stderr)
         return 2
 
     import torch

@@ -27,7 +27,7 @@ plain textbook definition:
   * a ring buffer of C slots per stream and KV head where token t lives in
     slot t mod C.
 
-Readings chosen where the paper is silent (all listed in the design doc):
+Readings chosen where the paper is silent:
 interleaved pairs; per-axis theta with its own D_a; fp32 cos/sin tables from
 float64 libm; stored K = bf16(fp32(rot_fp64(k))) with round-to-nearest-even at
 both steps; attention reads the pre-step ring plus the chunk's own K/V (the
