@@ -29,7 +29,10 @@
 // Online softmax in base-2 units (queries arrive pre-scaled by
 // scale*log2(e)) with a lazily raised reference max m per row: m moves only
 // when a tile's max exceeds it by more than kTau, or at the row's first
-// visible key, so weights stay below 2^kTau and the O rescale is rare.
+// visible key, so weights stay below 2^kTau and the O rescale is rare. The
+// QK MFMA chain starts from -m in its accumulator, so the scores come out
+// already relative to m and each weight costs one exp2 and no subtraction;
+// a raise of m subtracts its step from the tile it was found in.
 #include "frt_launch.hpp"
 
 namespace frt {
@@ -209,6 +212,7 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
   float m = 0.f, lsum = 0.f;
   bool mset = false;
+  f32x16 negm = {};  // -m in every element: the accumulator the QK chain starts from
 
   // ---- tile bookkeeping (block-uniform, scalar, branch free) ----
   // tile t: first key (slot, or own index for t >= c01) and fast flag
@@ -297,14 +301,13 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int j = 0; j < 2; ++j) vfo[kb][j] = (l32 * 8 + ((4 * kb + 2 * j + h) ^ ((l32 >> 1) & 7))) * 8;
-  // S^T for the 64 keys of a K buffer
+  // S^T - m for the 64 keys of a K buffer
   auto qk = [&](const uint16_t *kt, f32x16 (&s)[2]) __attribute__((always_inline)) {
-    const f32x16 zero = {};
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       const uint16_t *kblk = kt + kb * 32 * D;
       s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-          *reinterpret_cast<const bf16x8 *>(kblk + kfo[0]), qf[0], zero, 0, 0, 0);
+          *reinterpret_cast<const bf16x8 *>(kblk + kfo[0]), qf[0], negm, 0, 0, 0);
 #pragma unroll
       for (int k = 1; k < D / 16; ++k)
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
@@ -345,9 +348,10 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
         s[kb][r] = ok ? s[kb][r] : kNegInf;
       }
   };
-  // raise the reference max when the tile's max exceeds it (rare, uniform branch)
-  auto rescale = [&](float mt) __attribute__((always_inline)) {
-    const float rel = mt - m;
+  // raise the reference max when the tile's max exceeds it (rare, uniform
+  // branch); mt is the max of the tile's scores sx, which are relative to m
+  auto rescale = [&](float mt, f32x16 (&sx)[2]) __attribute__((always_inline)) {
+    const float rel = mt;
     const bool need = rel > kTau || (!mset && mt != kNegInf);
     if (__ballot(need)) {
       const float delta = need ? rel : 0.f;
@@ -359,6 +363,12 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
       lsum *= alpha;
       m += delta;
       mset = mset || need;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) negm[r] = -m;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sx[kb][r] -= delta;
     }
   };
   const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
@@ -367,7 +377,7 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
-        pf[kb][r >> 3][r & 7] = (__bf16)__builtin_amdgcn_exp2f(s[kb][r] - m);
+        pf[kb][r >> 3][r & 7] = (__bf16)__builtin_amdgcn_exp2f(s[kb][r]);
     // row sum of the rounded weights the PV product uses
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -422,7 +432,7 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
       mask_tile(t + 1, snext);
       mt = row_max(snext);
     }
-    rescale(mt);
+    rescale(mt, snext);
     wait_dma();
     __syncthreads();
   };
@@ -436,7 +446,7 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
     __syncthreads();
     qk(ks0, sa);
     if (!tile_fast(0)) mask_tile(0, sa);
-    rescale(row_max(sa));
+    rescale(row_max(sa), sa);
     __syncthreads();  // K buffer 0 is refilled by the first step
 
     int t = 0;
