@@ -314,14 +314,13 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
             *reinterpret_cast<const bf16x8 *>(kblk + kfo[k]), qf[k], s[kb], 0, 0, 0);
     }
   };
-  // row max over the tile: three-input max tree, then the lane 32 away
+  // row max over the tile: one chain of three-input maxima (v_max3), then
+  // the lane 32 away
   auto row_max = [&](const f32x16 (&s)[2]) __attribute__((always_inline)) {
-    float mt = fmaxf(s[0][0], fmaxf(s[0][1], s[0][2]));
+    float mt = fmaxf(fmaxf(s[0][0], s[0][1]), s[0][2]);
 #pragma unroll
-    for (int i = 3; i < 31; i += 2) {
-      const float a = s[i >> 4][i & 15], c = s[(i + 1) >> 4][(i + 1) & 15];
-      mt = fmaxf(mt, fmaxf(a, c));
-    }
+    for (int i = 3; i < 31; i += 2)
+      mt = fmaxf(fmaxf(mt, s[i >> 4][i & 15]), s[(i + 1) >> 4][(i + 1) & 15]);
     mt = fmaxf(mt, s[1][15]);
     return max_pair32(mt);
   };

@@ -36,8 +36,11 @@ __device__ __forceinline__ uint32_t e4m3x4(float a, float b, float c, float d) {
   return __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
 }
 // The same for values already known to lie within +-448 (no clamp needed).
+// The first conversion fills the low half of a word whose high half the
+// second one overwrites, so its starting contents are free: a's own bits,
+// which saves clearing a register.
 __device__ __forceinline__ uint32_t e4m3x4_inrange(float a, float b, float c, float d) {
-  const uint32_t w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  const uint32_t w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)__float_as_uint(a), false);
   return __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
 }
 

@@ -28,6 +28,7 @@
 #include "frt_launch.hpp"
 
 namespace frt {
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 namespace {
 
@@ -303,10 +304,9 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_fp8_kernel(AttnFp8Params p
   // V fragment of d row 32*db + l32: 16 keys 16h.. of block kb (kb*32*D bytes on)
   const int vfo = l32 * 32 + 16 * (h ^ ((l32 >> 3) & 1));
   auto frag32 = [](const uint8_t *p0, const uint8_t *p1) __attribute__((always_inline)) {
-    const u32x4 a = *reinterpret_cast<const u32x4 *>(p0);
-    const u32x4 c = *reinterpret_cast<const u32x4 *>(p1);
-    return i32x8{(int)a[0], (int)a[1], (int)a[2], (int)a[3], (int)c[0], (int)c[1], (int)c[2],
-                 (int)c[3]};
+    const i32x4 a = *reinterpret_cast<const i32x4 *>(p0);
+    const i32x4 c = *reinterpret_cast<const i32x4 *>(p1);
+    return (i32x8)__builtin_shufflevector(a, c, 0, 1, 2, 3, 4, 5, 6, 7);
   };
   // raw S^T (q8 . k8) for the 64 keys of a K buffer
   auto qk = [&](const uint8_t *kt, f32x16 (&s)[2]) __attribute__((always_inline)) {
@@ -322,14 +322,13 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_fp8_kernel(AttnFp8Params p
             frag32(kblk + kfo[st][0], kblk + kfo[st][1]), qf[st], s[kb], 0, 0, 0, 0, 0, 0);
     }
   };
-  // row max of the raw scores over the tile, then the lane 32 away
+  // row max of the raw scores over the tile (one chain of three-input
+  // maxima), then the lane 32 away
   auto row_max = [&](const f32x16 (&s)[2]) __attribute__((always_inline)) {
-    float mt = fmaxf(s[0][0], fmaxf(s[0][1], s[0][2]));
+    float mt = fmaxf(fmaxf(s[0][0], s[0][1]), s[0][2]);
 #pragma unroll
-    for (int i = 3; i < 31; i += 2) {
-      const float a = s[i >> 4][i & 15], c = s[(i + 1) >> 4][(i + 1) & 15];
-      mt = fmaxf(mt, fmaxf(a, c));
-    }
+    for (int i = 3; i < 31; i += 2)
+      mt = fmaxf(fmaxf(mt, s[i >> 4][i & 15]), s[(i + 1) >> 4][(i + 1) & 15]);
     mt = fmaxf(mt, s[1][15]);
     return max_pair32(mt);
   };
