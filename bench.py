@@ -39,8 +39,9 @@ PEAK_FP8_TFLOPS = 5033.2    # MI355X dense fp8 MFMA (published 5.0 PFLOP/s)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published 8 TB/s)
 
 
-def visible_counts(wl, L: int):
-    """Number of keys each query i of a stream holding L tokens attends to."""
+def visible_spans(wl, L: int):
+    """Inclusive visible key-token range [lo, hi] of each query i of a stream
+    holding L tokens (empty where hi < lo)."""
     i = np.arange(wl.n, dtype=np.int64)
     p = L + i
     if wl.mask.kind == MASK_BLOCK_CAUSAL:
@@ -54,6 +55,12 @@ def visible_counts(wl, L: int):
     present_hi = L + wl.n - 1
     lo = np.maximum(lo, present_lo)
     hi = np.minimum(hi, present_hi)
+    return lo, hi
+
+
+def visible_counts(wl, L: int):
+    """Number of keys each query i of a stream holding L tokens attends to."""
+    lo, hi = visible_spans(wl, L)
     return np.maximum(hi - lo + 1, 0)
 
 
@@ -63,10 +70,14 @@ def step_work(wl, lengths, kv_elem_bytes: int = 2):
     flops = 0
     kv_bytes = 0
     for L in lengths:
-        cnt = visible_counts(wl, int(L))
-        flops += int(cnt.sum()) * 4 * wl.d * wl.Hq
-        # distinct keys read by the stream: union over queries
-        kv_bytes += int(cnt.max()) * wl.Hkv * wl.d * 2 * kv_elem_bytes
+        lo, hi = visible_spans(wl, int(L))
+        live = hi >= lo
+        flops += int((hi - lo + 1)[live].sum()) * 4 * wl.d * wl.Hq
+        # distinct keys read by the stream: the union of the queries' ranges,
+        # which is one range (the ranges' ends never decrease with i)
+        if live.any():
+            union = int(hi[live].max() - lo[live].min() + 1)
+            kv_bytes += union * wl.Hkv * wl.d * 2 * kv_elem_bytes
     qo_bytes = 2 * wl.B * wl.n * wl.Hq * wl.d * 2
     return flops, kv_bytes + qo_bytes
 
