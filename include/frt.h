@@ -224,15 +224,17 @@ int32_t frt_decode_max_splits(const frt_ring *ring);
 
 /* Workspace bytes frt_decode_attn needs: an fp32 partial (max, sum, output
  * per query head of the group) for each of frt_decode_max_splits pieces and
- * one per (stream, KV head) holding the step's own token. */
+ * one per (stream, KV head) holding the step's own token. Its contents need
+ * no initialisation; calls sharing a workspace must be ordered on one
+ * stream. */
 size_t frt_decode_workspace_bytes(const frt_ring *ring, int32_t num_q_heads);
 
 /*
  * One-token decode step for every stream: frt_stream_attn_step with
  * n_new = 1, computed as split-KV (each piece of the visible ring tokens, and
  * the own token on its own, yields a partial max/sum/output per query head)
- * followed by a combine pass. Same tensor layouts with n_new = 1.
- * num_q_heads / num_kv_heads must be <= 16.
+ * followed by a combine pass, one block per (stream, KV head). Same tensor
+ * layouts with n_new = 1. num_q_heads / num_kv_heads must be <= 16.
  */
 frt_status frt_decode_attn(const frt_ring *ring, const frt_rope *rope,
                            const frt_mask *mask, const void *q,
@@ -366,13 +368,18 @@ const char *frt_last_error(void);
 
 /*
  * Built-in kernel timing. When enabled, every kernel the library launches
- * is bracketed by HIP events on its stream. frt_timing_query waits for the
- * recorded events of `kernel` (one of "rope_append", "seq_advance",
- * "chunk_prep", "chunk_attn", "chunk_append", "decode_split", "decode_combine") and returns
- * their count and summed milliseconds; frt_timing_reset drops all records.
+ * records its own start and end in a pair of HIP events on its stream.
+ * frt_timing_query waits for the recorded events of `kernel` (a launch name:
+ * "rope_append", "seq_advance", "chunk_prep", "chunk_attn", "chunk_append",
+ * "decode_split", "decode_combine"; the FP8 calls use the names of their
+ * bf16 counterparts) and returns their count and summed milliseconds. frt_timing_samples writes the duration of each of
+ * them, in launch order, to ms_out (at most `capacity` values) and the number
+ * recorded to *count. frt_timing_reset drops all records.
  */
 frt_status frt_timing_enable(int32_t on);
 frt_status frt_timing_query(const char *kernel, int32_t *count, double *total_ms);
+frt_status frt_timing_samples(const char *kernel, float *ms_out, int32_t capacity,
+                              int32_t *count);
 void frt_timing_reset(void);
 
 #ifdef __cplusplus

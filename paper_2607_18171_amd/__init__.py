@@ -10,7 +10,7 @@ from .binding import (FrtError, Ring, Rope, mask, kv_append, stream_attn_step,
                       RingFp8, kv_append_fp8, stream_attn_fp8_workspace_bytes,
                       stream_attn_step_fp8, stream_step_fp8, decode_fp8_workspace_bytes,
                       decode_attn_fp8, decode_step_fp8, decode_step, decode_workspace_bytes,
-                      decode_max_splits, timing_enable, timing_query, timing_reset,
+                      decode_max_splits, timing_enable, timing_query, timing_samples, timing_reset,
                       load_library, ROPE_NONE, ROPE_1D, ROPE_3D, MASK_BLOCK_CAUSAL,
                       MASK_CAUSAL, EXPORTS, LIB_PATH)
 
@@ -21,6 +21,6 @@ __all__ = [
     "decode_fp8_workspace_bytes", "decode_attn_fp8", "decode_step_fp8",
     "decode_step",
     "decode_workspace_bytes", "decode_max_splits",
-    "timing_enable", "timing_query", "timing_reset", "load_library", "ROPE_NONE", "ROPE_1D",
+    "timing_enable", "timing_query", "timing_samples", "timing_reset", "load_library", "ROPE_NONE", "ROPE_1D",
     "ROPE_3D", "MASK_BLOCK_CAUSAL", "MASK_CAUSAL", "EXPORTS", "LIB_PATH",
 ]

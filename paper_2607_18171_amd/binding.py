@@ -33,7 +33,7 @@ EXPORTS = (
     "frt_decode_fp8_workspace_bytes", "frt_decode_attn_fp8", "frt_decode_step_fp8",
     "frt_status_str",
     "frt_last_error",
-    "frt_timing_enable", "frt_timing_query", "frt_timing_reset",
+    "frt_timing_enable", "frt_timing_query", "frt_timing_samples", "frt_timing_reset",
 )
 
 
@@ -113,6 +113,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "frt_timing_enable": (I32, [I32]),
         "frt_timing_query": (I32, [ctypes.c_char_p, ctypes.POINTER(I32),
                                    ctypes.POINTER(ctypes.c_double)]),
+        "frt_timing_samples": (I32, [ctypes.c_char_p, ctypes.POINTER(ctypes.c_float), I32,
+                                     ctypes.POINTER(I32)]),
         "frt_timing_reset": (None, []),
     }
     for name, (res, args) in sig.items():
@@ -411,6 +413,15 @@ def timing_query(kernel: str):
     ms = ctypes.c_double(0.0)
     _check(load_library().frt_timing_query(kernel.encode(), ctypes.byref(c), ctypes.byref(ms)))
     return c.value, ms.value
+
+
+def timing_samples(kernel: str):
+    """Durations (ms) of the recorded launches of `kernel`, in launch order."""
+    c = ctypes.c_int32(0)
+    _check(load_library().frt_timing_samples(kernel.encode(), None, 0, ctypes.byref(c)))
+    buf = (ctypes.c_float * max(c.value, 1))()
+    _check(load_library().frt_timing_samples(kernel.encode(), buf, c.value, ctypes.byref(c)))
+    return [float(buf[i]) for i in range(c.value)]
 
 
 def timing_reset() -> None:

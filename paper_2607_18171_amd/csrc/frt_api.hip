@@ -828,6 +828,28 @@ frt_status frt_timing_query(const char *kernel, int32_t *count, double *total_ms
   return FRT_OK;
 }
 
+frt_status frt_timing_samples(const char *kernel, float *ms_out, int32_t capacity,
+                              int32_t *count) {
+  if (!kernel || !count || (capacity > 0 && !ms_out))
+    return fail(FRT_ERR_NULL, "timing samples argument is NULL");
+  std::lock_guard<std::mutex> lk(g_tmu);
+  int c = 0;
+  for (const TimingRec &r : g_recs) {
+    if (std::strcmp(r.name, kernel) != 0) continue;
+    if (c < capacity) {
+      if (hipEventSynchronize(r.stop) != hipSuccess)
+        return fail(FRT_ERR_HIP, "hipEventSynchronize failed");
+      float ms = 0.f;
+      if (hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess)
+        return fail(FRT_ERR_HIP, "hipEventElapsedTime failed");
+      ms_out[c] = ms;
+    }
+    ++c;
+  }
+  *count = c;
+  return FRT_OK;
+}
+
 void frt_timing_reset(void) {
   std::lock_guard<std::mutex> lk(g_tmu);
   for (const TimingRec &r : g_recs) {

@@ -354,7 +354,9 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
     const bool need = rel > kTau || (!mset && mt != kNegInf);
     if (__ballot(need)) {
       const float delta = need ? rel : 0.f;
-      const float alpha = __builtin_amdgcn_exp2f(-delta);
+      // a row's first visible tile finds O and the sum still zero: alpha = 1
+      // there, since exp2(-delta) overflows for a tile max below -128
+      const float alpha = mset ? __builtin_amdgcn_exp2f(-delta) : 1.f;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
 #pragma unroll

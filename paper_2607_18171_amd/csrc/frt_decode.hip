@@ -17,19 +17,22 @@
 // so the V^T operand of O^T = V^T P^T is one 16-byte load (8 consecutive
 // tokens start at a slot that is a multiple of 8, and C is too, so they never
 // wrap or leave their V block). With C a multiple of 32 a tile is exactly one
-// V block: 64*D contiguous bytes. Combine pass: one block per (query head, KV head, stream) rescales
-// the head's live partials to their common max and normalises.
+// V block: 64*D contiguous bytes. Combine pass: one block per (stream, KV
+// head) loads the head's partials in groups, rescales them to their common
+// max and normalises.
 #include "frt_decode_pieces.hpp"
 
 namespace frt {
 
 namespace {
 
-// Own-token partial slot (32-bit words): max[G], sum[G] (= 1), then the
-// head's piece range {K, np}, the query token L as two words, and the key as
-// the ring stores it (D/2 words of bf16 pairs). Its output row is v_new,
-// which the combine pass reads from the input.
+// Own-token partial slot (32-bit words): max[G], sum[G] (= 1), then, where a
+// piece's outputs start, the head's piece range {K, np}, the query token L as
+// two words, and the key as the ring stores it (D/2 words of bf16 pairs). Its
+// output row is v_new, which the combine pass reads from the input.
 constexpr int kOwnHdr = 4;
+
+constexpr bf16x2 kOnes2 = {(__bf16)1.f, (__bf16)1.f};
 
 template <int D>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecWavesPerSimd))) void decode_split_kernel(
@@ -94,7 +97,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecWavesPe
     int K, np;
     head_pieces(p, lane, b, kvh, K, np);
     float *part = p.ws + (size_t)(p.nwaves + h) * pfl;
-    uint32_t *hdr = reinterpret_cast<uint32_t *>(part + 2 * G);
+    uint32_t *hdr = reinterpret_cast<uint32_t *>(part + decode_out_off(G));
     if (c16 < G && g4 == 0) {
       part[c16] = so;
       part[G + c16] = 1.f;
@@ -244,15 +247,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecWavesPe
         const float alpha = __builtin_amdgcn_exp2f(m - msafe);
         m = mnew;
         bf16x8 pf;
-        float ts = 0.f;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float e = __builtin_amdgcn_exp2f(sacc[kb][r] - msafe);
-            ts += e;
-            pf[4 * kb + r] = (__bf16)e;
-          }
+          for (int r = 0; r < 4; ++r)
+            pf[4 * kb + r] = (__bf16)__builtin_amdgcn_exp2f(sacc[kb][r] - msafe);
+        // the sum takes the rounded weights the PV product uses, so that the
+        // output is a convex combination of the V rows
+        float ts = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const bf16x2 pr = {pf[2 * w], pf[2 * w + 1]};
+          ts = __builtin_amdgcn_fdot2_f32_bf16(pr, kOnes2, ts, false);
+        }
         lsum = lsum * alpha + ts;
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
@@ -270,11 +277,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecWavesPe
     lsum += __shfl_xor(lsum, 32);
     float *part = p.ws + (size_t)wv * pfl;
     if (c16 < G) {
-      float *orow = part + 2 * G + c16 * D;
+      float *orow = part + decode_out_off(G) + c16 * D;
 #pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) orow[16 * db + 4 * g4 + r] = o[db][r];
+      for (int db = 0; db < NDB; ++db) *reinterpret_cast<f32x4 *>(orow + 16 * db + 4 * g4) = o[db];
       if (g4 == 0) {
         part[c16] = m;
         part[G + c16] = lsum;
@@ -284,83 +289,119 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecWavesPe
   }
 }
 
-// Combine pass: one block of D threads per (query head, KV head, stream);
-// thread d owns output column d. The head's partials are its pieces (their
-// slot range is recorded in the own-token slot by the split pass) and its
-// own-token partial. Partials
-// are merged online in groups of kCombineGroup: the (max, sum, column) loads
-// of a group are independent, so after the stream lengths are known the pass
-// waits on memory once per group.
+// Combine pass: one block of kCombineThreads threads per (stream, KV head).
+// Thread t owns the 4-float groups t, t + kCombineThreads, ... of the head's
+// G x D outputs (query g = group / (D/4)). The head's partials are its pieces
+// (their slot range is recorded in the own-token slot by the split pass) and
+// its own-token partial; they are merged online in groups of kCombineGroup,
+// whose (max, sum, outputs) loads are independent, so the pass waits on
+// memory once for the own-token slot and once per group.
+constexpr int kCombineThreads = 256;
 constexpr int kCombineGroup = 16;
 
-template <int D>
-__global__ __launch_bounds__(D) void decode_combine_kernel(DecodeParams p) {
-  const int q = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+template <int D, int F>
+__global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeParams p) {
+  constexpr int Q4 = D / 4;  // 4-float groups per output row
+  const int kvh = blockIdx.x, b = blockIdx.y;
   const int t = threadIdx.x;
   const int G = p.G;
   const int head = b * p.Hkv + kvh;
-  const int hq = kvh * G + q;
   const size_t pstride = decode_split_floats(G, D);
+  const int oo = decode_out_off(G);
 
-  // the head's pieces (slots K .. K+np-1) and query token, as the split
-  // pass recorded them in the own-token slot; seq_len is not read here, so
-  // that an appending combine may advance it
+  // the head's pieces (slots K .. K+np-1) and query token, as the split pass
+  // recorded them in the own-token slot; seq_len is not read here, so that an
+  // appending combine may advance it
   const float *own = p.ws + (size_t)(p.nwaves + head) * pstride;
-  const uint32_t *hdr = reinterpret_cast<const uint32_t *>(own + 2 * G);
+  const uint32_t *hdr = reinterpret_cast<const uint32_t *>(own + oo);
   const int K = (int)hdr[0], np = (int)hdr[1];
   const long long L = (long long)((unsigned long long)hdr[2] | ((unsigned long long)hdr[3] << 32));
-  const int ncand = np + 1;  // pieces, then the own token
 
-  float M = kNegInf, acc = 0.f, lt = 0.f;
-  for (int c0 = 0; c0 < ncand; c0 += kCombineGroup) {
-    float mv[kCombineGroup], lv[kCombineGroup], ov[kCombineGroup];
+  int gq[F], e4[F];  // query and first element of each of this thread's groups
+  bool live[F];
+#pragma unroll
+  for (int f = 0; f < F; ++f) {
+    const int idx = t + kCombineThreads * f;
+    live[f] = idx < G * Q4;
+    gq[f] = live[f] ? idx / Q4 : 0;
+    e4[f] = live[f] ? 4 * (idx % Q4) : 0;
+  }
+  float M[F], lt[F];
+  f32x4 acc[F];
+#pragma unroll
+  for (int f = 0; f < F; ++f) {
+    M[f] = kNegInf;
+    lt[f] = 0.f;
+    acc[f] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int c0 = 0; c0 <= np; c0 += kCombineGroup) {
+    float mv[kCombineGroup][F], lv[kCombineGroup][F];
+    f32x4 ov[kCombineGroup][F];
 #pragma unroll
     for (int j = 0; j < kCombineGroup; ++j) {
       const int c = c0 + j;
-      mv[j] = kNegInf;
-      lv[j] = 0.f;
-      ov[j] = 0.f;
-      if (c < np) {
-        const float *pp = p.ws + (size_t)(K + c) * pstride;
-        mv[j] = pp[q];
-        lv[j] = pp[G + q];
-        ov[j] = pp[2 * G + q * D + t];
-      } else if (c == np) {
-        mv[j] = own[q];
-        lv[j] = own[G + q];
-        ov[j] = bf16_bits_to_f32(p.v_new[(size_t)head * D + t]);
+#pragma unroll
+      for (int f = 0; f < F; ++f) {
+        mv[j][f] = kNegInf;
+        lv[j][f] = 0.f;
+        ov[j][f] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (c < np) {
+          const float *pp = p.ws + (size_t)(K + c) * pstride;
+          mv[j][f] = pp[gq[f]];
+          lv[j][f] = pp[G + gq[f]];
+          ov[j][f] = *reinterpret_cast<const f32x4 *>(pp + oo + gq[f] * D + e4[f]);
+        } else if (c == np) {
+          mv[j][f] = own[gq[f]];
+          lv[j][f] = own[G + gq[f]];
+          const u32x2 w = *reinterpret_cast<const u32x2 *>(p.v_new + (size_t)head * D + e4[f]);
+          ov[j][f] = f32x4{bf16_bits_to_f32(w[0] & 0xffffu), bf16_bits_to_f32(w[0] >> 16),
+                           bf16_bits_to_f32(w[1] & 0xffffu), bf16_bits_to_f32(w[1] >> 16)};
+        }
       }
     }
-    // live partials have a positive sum (the own token's always has)
-    float Mg = M;
 #pragma unroll
-    for (int j = 0; j < kCombineGroup; ++j) Mg = lv[j] > 0.f ? fmaxf(Mg, mv[j]) : Mg;
-    if (Mg != kNegInf) {
-      const float a = __builtin_amdgcn_exp2f(M - Mg);  // M = -inf gives 0
-      acc *= a;
-      lt *= a;
+    for (int f = 0; f < F; ++f) {
+      // live partials have a positive sum (the own token's always has)
+      float Mg = M[f];
 #pragma unroll
-      for (int j = 0; j < kCombineGroup; ++j) {
-        const float w = lv[j] > 0.f ? __builtin_amdgcn_exp2f(mv[j] - Mg) : 0.f;
-        acc += ov[j] * w;
-        lt += lv[j] * w;
+      for (int j = 0; j < kCombineGroup; ++j) Mg = lv[j][f] > 0.f ? fmaxf(Mg, mv[j][f]) : Mg;
+      if (Mg != kNegInf) {
+        const float a = __builtin_amdgcn_exp2f(M[f] - Mg);  // M = -inf gives 0
+        acc[f] *= a;
+        lt[f] *= a;
+#pragma unroll
+        for (int j = 0; j < kCombineGroup; ++j) {
+          const float w = lv[j][f] > 0.f ? __builtin_amdgcn_exp2f(mv[j][f] - Mg) : 0.f;
+          acc[f] += ov[j][f] * w;
+          lt[f] += lv[j][f] * w;
+        }
+        M[f] = Mg;
       }
-      M = Mg;
     }
   }
-  p.out[((size_t)b * p.Hq + hq) * D + t] = (uint16_t)f32_to_bf16_rne(acc / lt);
-  if (t == 0 && p.lse != nullptr)
-    p.lse[(size_t)b * p.Hq + hq] = (M + __builtin_amdgcn_logf(lt)) * 0.6931471805599453f;
+#pragma unroll
+  for (int f = 0; f < F; ++f) {
+    if (!live[f]) continue;
+    const float inv = 1.f / lt[f];
+    const int hq = kvh * G + gq[f];
+    u32x2 w;
+    w[0] = f32_to_bf16_rne(acc[f][0] * inv) | (f32_to_bf16_rne(acc[f][1] * inv) << 16);
+    w[1] = f32_to_bf16_rne(acc[f][2] * inv) | (f32_to_bf16_rne(acc[f][3] * inv) << 16);
+    *reinterpret_cast<u32x2 *>(p.out + ((size_t)b * p.Hq + hq) * D + e4[f]) = w;
+    if (e4[f] == 0 && p.lse != nullptr)
+      p.lse[(size_t)b * p.Hq + hq] = (M[f] + __builtin_amdgcn_logf(lt[f])) * 0.6931471805599453f;
+  }
 
   // the append: the split pass has finished every read of the ring and of
   // seq_len, and no combine block reads either
-  if (p.append && q == 0) {
+  if (p.append) {
     const int slot = (int)(L % p.C);
     if (t < D / 2)
       reinterpret_cast<uint32_t *>(p.k_ring + ((size_t)head * p.C + slot) * D)[t] =
           hdr[kOwnHdr + t];
-    p.v_ring[(size_t)head * D * p.C + vring_elem(slot, t, p.C, D)] =
-        p.v_new[(size_t)head * D + t];
+    if (t < D)
+      p.v_ring[(size_t)head * D * p.C + vring_elem(slot, t, p.C, D)] =
+          p.v_new[(size_t)head * D + t];
     if (kvh == 0 && t == 0) p.seq_len[b] = L + 1;
   }
 }
@@ -378,11 +419,14 @@ hipError_t launch_decode_split(const DecodeParams &p, const RopeDev &r, hipStrea
 }
 
 hipError_t launch_decode_combine(const DecodeParams &p, hipStream_t s) {
-  dim3 grid(p.G, p.Hkv, p.B);
-  if (p.D == 128)
-    dispatch(decode_combine_kernel<128>, grid, dim3(128), s, p);
+  dim3 grid(p.Hkv, p.B);
+  const bool two = p.G * p.D / 4 > kCombineThreads;  // at most 2 groups of 4 per thread
+  if (p.D == 128 && two)
+    dispatch(decode_combine_kernel<128, 2>, grid, dim3(kCombineThreads), s, p);
+  else if (p.D == 128)
+    dispatch(decode_combine_kernel<128, 1>, grid, dim3(kCombineThreads), s, p);
   else
-    dispatch(decode_combine_kernel<64>, grid, dim3(64), s, p);
+    dispatch(decode_combine_kernel<64, 1>, grid, dim3(kCombineThreads), s, p);
   return hipGetLastError();
 }
 

@@ -153,7 +153,6 @@ constexpr int kDecBufs = 2;          // decode split tiles in flight per wave
 constexpr int kDecResident = 256 * 4 * kDecWavesPerSimd;  // split waves resident at once
 constexpr int kDecChunk = 12;        // most 32-token tiles of one decode piece
 
-// Floats of one decode partial: max[G], sum[G], out[G][D].
 // Piece waves of a decode call: enough for every split of the tiles
 // (resident waves plus one per head, or pieces of kDecChunk tiles when the
 // ring is long), rounded up to whole blocks of 4 waves.
@@ -165,7 +164,13 @@ __host__ __device__ inline int decode_piece_waves(int B, int Hkv, int C) {
   w = w > cap ? w : cap;
   return (int)((w + 3) / 4 * 4);
 }
-__host__ __device__ inline size_t decode_split_floats(int G, int D) { return (size_t)G * (2 + D); }
+// One decode partial (floats): max[G] at 0, sum[G] at G, out[G][D] from
+// decode_out_off(G); the stride keeps every partial and its output rows
+// 16-byte aligned.
+__host__ __device__ inline int decode_out_off(int G) { return (2 * G + 3) / 4 * 4; }
+__host__ __device__ inline size_t decode_split_floats(int G, int D) {
+  return (size_t)decode_out_off(G) + (size_t)G * D;
+}
 // Floats of one FP8 decode partial: max[G], sum[G], out[G][D], then (in a
 // head's own-token slot) 4 header words and the token's key and value codes.
 __host__ __device__ inline size_t decode_fp8_split_floats(int G, int D) {

@@ -30,7 +30,7 @@ def declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = frt.load_library()
     names = declared_symbols()
-    assert len(names) == 22
+    assert len(names) == 23
     for name in names:
         assert hasattr(lib, name), name
     assert sorted(B.EXPORTS) == names
@@ -111,10 +111,11 @@ def test_decode_rejects_bad_arguments():
     o = rope()
     wsb = lib.frt_decode_workspace_bytes(ctypes.byref(r), 8)
     # piece waves: the resident count (2048) plus one per (stream, KV head),
-    # rounded up to blocks of 4; the workspace adds one own-token partial per head
+    # rounded up to blocks of 4; the workspace adds one own-token partial per
+    # head (a partial: max[8], sum[8], out[8][128] floats)
     waves = lib.frt_decode_max_splits(ctypes.byref(r))
     assert waves == (2048 + 1 + 3) // 4 * 4
-    assert wsb == (waves + 1) * 8 * (2 + 128) * 4
+    assert wsb == (waves + 1) * (16 + 8 * 128) * 4
 
     for fn in (lib.frt_decode_attn, lib.frt_decode_step):
         def dec(hq=8, ws=FAKE, n=wsb):

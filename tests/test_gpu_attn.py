@@ -193,3 +193,60 @@ def test_stream_step_equals_attn_then_append(name):
         assert torch.equal(ring.seq_len, twin.seq_len), (name, s)
         oring = oracle.kv_append(oring, kn, vn, wl.rope)
     assert ring_bytes_equal(ring, oring)
+
+
+def test_very_negative_first_tile():
+    """Every row's first visible tile scores below -128 in base-2 units (its keys
+    point against the query), the later keys are ordinary: the output is the
+    oracle's, not the 0 * inf of rescaling an empty accumulator by exp2(-max)."""
+    wl = shrink(WORKLOADS["prefill_swa"], B=1, Hq=2, Hkv=1, n=64, C=256,
+                rope=RopeSpec(ROPE_NONE), mask=MaskSpec(MASK_CAUSAL, 0, 0))
+    case = make_case(wl, 9, lengths=np.array([160]))
+    four = 0x4080  # bf16 4.0
+    case.q[:] = four
+    k0, _ = case.prior_fills[0]
+    k0[:, :64] = four | 0x8000  # tokens 0..63: -4 in every dim, q.k*scale = -181
+    small = draw_bf16(np.random.default_rng(3), k0[:, 64:].shape, 0.05)
+    k0[:, 64:] = small
+    case.k_new[:] = draw_bf16(np.random.default_rng(4), case.k_new.shape, 0.05)
+    ring, oring, rope = build_rings(case)
+    out, lse = run_step(case, ring, rope)
+    ref, ref_lse = oracle.stream_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask)
+    check_close(bf16_dev_to_f64(out), ref, visible_vmax(oring, case), "negative first tile")
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() < 2e-2
+
+
+@pytest.mark.parametrize("name,j", [("gqa_swa", 57), ("mha_causal", 20), ("gqa_d64", 64)])
+def test_future_own_token_has_no_influence(name, j):
+    """Causal mask: changing the chunk's own token j (its key and value) leaves the
+    outputs and LSE of every query i < j bit for bit unchanged."""
+    wl = SMALL[name]
+    case = make_case(wl, 13)
+    ring, oring, rope = build_rings(case)
+    out_a, lse_a = run_step(case, ring, rope)
+    rng = np.random.default_rng(14)
+    case.k_new[:, j] = draw_bf16(rng, case.k_new[:, j].shape, 3.0)
+    case.v_new[:, j] = draw_bf16(rng, case.v_new[:, j].shape, 3.0)
+    out_b, lse_b = run_step(case, ring, rope)
+    a, b = out_a.view(torch.int16), out_b.view(torch.int16)
+    assert torch.equal(a[:, :j], b[:, :j])
+    assert torch.equal(lse_a[:, :, :j], lse_b[:, :, :j])
+    assert not torch.equal(a[:, j:], b[:, j:])  # the later queries do see it
+
+
+@pytest.mark.parametrize("C2", [264, 333 - 333 % 8])
+def test_ring_capacity_does_not_change_the_result(C2):
+    """The same token stream in rings of 256 and of C2 slots (the tokens sit at other
+    physical slots, and the tiles cut the visible keys elsewhere): both results
+    within tolerance of the oracle, and the oracle's two results equal up to fp64
+    rounding (the larger ring holds more, invisible, tokens)."""
+    outs = []
+    for C in (256, C2):
+        wl = shrink(SMALL["gqa_swa"], C=C)
+        case = make_case(wl, 15, lengths=np.array([0, 300, 750]))
+        ring, oring, rope = build_rings(case)
+        out, _ = run_step(case, ring, rope)
+        ref, _ = oracle.stream_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask)
+        check_close(bf16_dev_to_f64(out), ref, visible_vmax(oring, case), "C%d" % C)
+        outs.append(ref)
+    assert np.abs(outs[0] - outs[1]).max() <= 1e-12

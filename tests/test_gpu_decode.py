@@ -95,3 +95,72 @@ def test_decode_step_equals_attn_then_append(name):
         assert torch.equal(ring.seq_len, twin.seq_len), (name, s)
         oring = oracle.kv_append(oring, kn, vn, wl.rope)
     assert ring_bytes_equal(ring, oring)
+
+
+def test_decode_v_all_ones_gives_ones():
+    """V = 1 everywhere: the output is a convex combination of ones, so 1 within one bf16
+    step (the sum uses the same rounded weights as the P.V product)."""
+    wl, lengths = CASES["split_edges"]
+    case = make_case(wl, 7, lengths=np.array(lengths))
+    case.v_new[:] = 0x3F80
+    for _, v in case.prior_fills:
+        v[:] = 0x3F80
+    ring, oring, rope = build_rings(case)
+    out, _ = run_decode(case, ring, rope)
+    assert np.abs(bf16_dev_to_f64(out) - 1.0).max() <= 4e-3
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("Hq,Hkv", [(3, 3), (4, 2), (6, 2), (8, 2), (10, 2), (16, 2), (32, 2)])
+def test_decode_group_sizes(Hq, Hkv, d):
+    """Every query-group size G = Hq/Hkv from 1 to 16 (the combining wave splits its
+    lanes over the G x d outputs by G), at both head dims."""
+    wl = shrink(WORKLOADS["decode"], B=3, Hq=Hq, Hkv=Hkv, d=d, C=704,
+                rope=RopeSpec(ROPE_1D, (d, 0, 0)))
+    case = make_case(wl, Hq + d, lengths=np.array([703, 0, 333]))
+    ring, oring, rope = build_rings(case)
+    out, lse = run_decode(case, ring, rope)
+    ref, ref_lse = oracle.decode_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask)
+    check_close(bf16_dev_to_f64(out), ref, visible_vmax(oring, case), "G%d d%d" % (Hq // Hkv, d))
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() < 2e-2
+
+
+def _pieces_per_head(wl, lengths):
+    """Pieces the decode pass cuts each (stream, KV head) of these lengths into: the
+    visible ring tokens as 32-token tiles (causal, no window: tokens 0 .. L-1), `per`
+    tiles a piece with per = clamp(ceil(T / slots), 4, 12), T the tiles of every head
+    and slots the 2048 resident waves less one per head."""
+    tiles = [(L + 31) // 32 for L in lengths]
+    heads = len(lengths) * wl.Hkv
+    T = sum(tiles) * wl.Hkv
+    slots = max(2048 - heads, 1024)
+    per = min(max(-(-T // slots), 4), 12)
+    return [-(-t // per) for t in tiles]
+
+
+def test_decode_split_count_independence():
+    """The same stream decoded alone and inside batches whose total work cuts its
+    ring into different numbers of pieces: each result within tolerance of the
+    oracle (the split is an exact rewrite of the definition)."""
+    L0 = 6000
+    base = shrink(WORKLOADS["decode"], B=1, C=8448)
+    one = make_case(base, 21, lengths=np.array([L0]))
+    splits = set()
+    for B in (1, 12, 24):
+        wl = shrink(WORKLOADS["decode"], B=B, C=8448)
+        lengths = np.array([L0] + [8000] * (B - 1))
+        case = make_case(wl, 22 + B, lengths=lengths)
+        # stream 0 carries exactly the single-stream case's data
+        case.prior_fills[0] = one.prior_fills[0]
+        case.q[0] = one.q[0]
+        case.k_new[0] = one.k_new[0]
+        case.v_new[0] = one.v_new[0]
+        splits.add(_pieces_per_head(wl, lengths)[0])
+        ring, oring, rope = build_rings(case)
+        out, lse = run_decode(case, ring, rope)
+        ref, ref_lse = oracle.decode_attn(oring, case.q[:1], case.k_new[:1], case.v_new[:1],
+                                          wl.rope, wl.mask)
+        got = bf16_dev_to_f64(out)[:1]
+        check_close(got, ref, visible_vmax(oring, case), "B%d" % B)
+        assert np.abs(lse.cpu().numpy()[:1] - ref_lse).max() < 2e-2
+    assert len(splits) == 3, splits

@@ -189,3 +189,57 @@ def test_row_subset_equals_full():
     sub, lse2 = oracle.stream_attn(ring, q, k, v, R1D, mask, rows=rows)
     assert np.array_equal(sub[:, rows], full[:, rows])
     assert np.array_equal(lse2[:, :, rows], lse[:, :, rows])
+
+
+@pytest.mark.parametrize("shift", [1, 7, 23])
+def test_physical_ring_rotation_does_not_change_the_result(shift):
+    """The same visible keys at another physical offset: ring B first takes `shift`
+    tokens that end up outside the causal window, then the same token values as
+    ring A, so every slot holds A's value `shift` slots further on. Without RoPE
+    and under a relative (causal-window) mask, the step's result is the same up to
+    fp64 rounding; an error in the slot <-> token map reads other keys in one of
+    the two rings and breaks it."""
+    rng = np.random.default_rng(30)
+    B, H, C, d, n, W = 1, 2, 24, 32, 5, 16
+    mask = MaskSpec(MASK_CAUSAL, 0, W)
+    toks_k = rand_bits(rng, (B, 40, H, d))
+    toks_v = rand_bits(rng, (B, 40, H, d))
+    junk_k = rand_bits(rng, (B, shift, H, d))
+    junk_v = rand_bits(rng, (B, shift, H, d))
+    q = rand_bits(rng, (B, n, H, d))
+    k = rand_bits(rng, (B, n, H, d))
+    v = rand_bits(rng, (B, n, H, d))
+    ra = oracle.new_ring(B, H, C, d)
+    for s in range(0, 40, 8):
+        ra = oracle.kv_append(ra, toks_k[:, s:s + 8], toks_v[:, s:s + 8], NONE)
+    rb = oracle.kv_append(oracle.new_ring(B, H, C, d), junk_k, junk_v, NONE)
+    for s in range(0, 40, 8):
+        rb = oracle.kv_append(rb, toks_k[:, s:s + 8], toks_v[:, s:s + 8], NONE)
+    # same values, slots rotated by `shift`
+    assert np.array_equal(np.roll(ra.k, shift, axis=2), rb.k)
+    oa, la = oracle.stream_attn(ra, q, k, v, NONE, mask)
+    ob, lb = oracle.stream_attn(rb, q, k, v, NONE, mask)
+    assert np.abs(oa - ob).max() <= 1e-12
+    assert np.abs(la - lb).max() <= 1e-12
+
+
+def test_ring_capacity_beyond_the_window_does_not_change_the_result():
+    """One token stream in rings of C = window - 1 (the least a causal window of W
+    keys needs) and of larger capacities: equal results up to fp64 rounding."""
+    rng = np.random.default_rng(31)
+    B, H, d, n, W = 2, 2, 32, 6, 20
+    mask = MaskSpec(MASK_CAUSAL, 0, W)
+    kk = rand_bits(rng, (B, 50, H, d))
+    vv = rand_bits(rng, (B, 50, H, d))
+    q = rand_bits(rng, (B, n, H, d))
+    k = rand_bits(rng, (B, n, H, d))
+    v = rand_bits(rng, (B, n, H, d))
+    outs = []
+    for C in (W - 1, W + 5, 64):
+        ring = oracle.new_ring(B, H, C, d)
+        for s in range(0, 50, 10):
+            ring = oracle.kv_append(ring, kk[:, s:s + 10], vv[:, s:s + 10], R1D)
+        outs.append(oracle.stream_attn(ring, q, k, v, R1D, mask))
+    for o, l in outs[1:]:
+        assert np.abs(o - outs[0][0]).max() <= 1e-12
+        assert np.abs(l - outs[0][1]).max() <= 1e-12
