@@ -261,6 +261,27 @@ frt_status frt_decode_step(const frt_ring *ring, const frt_rope *rope,
                            float *lse, void *hip_stream);
 
 /*
+ * frt_decode_step without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation). The split partials live in a fixed
+ * device array of FRT_NOALLOC_SCRATCH_BYTES bytes inside the library, one per
+ * GPU, held until the process ends; the call allocates nothing. Calls on one
+ * GPU share that array, so calls that overlap on one GPU (different streams
+ * with no ordering between them) race and must not be made; calls ordered on
+ * one stream are fine. The stream must belong to the current device.
+ * Returns FRT_ERR_WORKSPACE when frt_decode_workspace_bytes(ring,
+ * num_q_heads) exceeds FRT_NOALLOC_SCRATCH_BYTES (e.g. 32 streams x 4 KV
+ * heads x 8 query heads per KV head at head_dim 128 need 9.6 MB), otherwise
+ * behaves exactly as frt_decode_step.
+ */
+#define FRT_NOALLOC_SCRATCH_BYTES (32u << 20)
+frt_status frt_decode_step_noalloc(const frt_ring *ring, const frt_rope *rope,
+                                   const frt_mask *mask, const void *q,
+                                   const void *k_new, const void *v_new,
+                                   int32_t num_q_heads, float softmax_scale,
+                                   void *out, float *lse, void *hip_stream);
+
+/*
  * FP8 variant (the FP8 KV cache with FP8 Q.K^T and P.V). The ring holds
  * OCP e4m3fn codes (1 sign, 4 exponent bits with bias 7, 3 mantissa bits;
  * largest finite 448, 0x7f / 0xff NaN), same layouts as above with one-byte

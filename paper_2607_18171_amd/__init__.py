@@ -9,7 +9,8 @@ from .binding import (FrtError, Ring, Rope, mask, kv_append, stream_attn_step,
                       stream_attn_workspace_bytes, stream_step, decode_attn,
                       RingFp8, kv_append_fp8, stream_attn_fp8_workspace_bytes,
                       stream_attn_step_fp8, stream_step_fp8, decode_fp8_workspace_bytes,
-                      decode_attn_fp8, decode_step_fp8, decode_step, decode_workspace_bytes,
+                      decode_attn_fp8, decode_step_fp8, decode_step, decode_step_noalloc,
+                      decode_workspace_bytes,
                       decode_max_splits, timing_enable, timing_query, timing_samples, timing_reset,
                       load_library, ROPE_NONE, ROPE_1D, ROPE_3D, MASK_BLOCK_CAUSAL,
                       MASK_CAUSAL, EXPORTS, LIB_PATH)
@@ -19,7 +20,7 @@ __all__ = [
     "stream_attn_workspace_bytes", "stream_step", "decode_attn", "RingFp8",
     "kv_append_fp8", "stream_attn_fp8_workspace_bytes", "stream_attn_step_fp8", "stream_step_fp8",
     "decode_fp8_workspace_bytes", "decode_attn_fp8", "decode_step_fp8",
-    "decode_step",
+    "decode_step", "decode_step_noalloc",
     "decode_workspace_bytes", "decode_max_splits",
     "timing_enable", "timing_query", "timing_samples", "timing_reset", "load_library", "ROPE_NONE", "ROPE_1D",
     "ROPE_3D", "MASK_BLOCK_CAUSAL", "MASK_CAUSAL", "EXPORTS", "LIB_PATH",

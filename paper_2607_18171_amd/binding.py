@@ -28,7 +28,8 @@ EXPORTS = (
     "frt_rope_table_bytes", "frt_rope_table_fill", "frt_kv_append",
     "frt_stream_attn_workspace_bytes", "frt_stream_attn_step", "frt_stream_step",
     "frt_decode_max_splits",
-    "frt_decode_workspace_bytes", "frt_decode_attn", "frt_decode_step", "frt_kv_append_fp8",
+    "frt_decode_workspace_bytes", "frt_decode_attn", "frt_decode_step", "frt_decode_step_noalloc",
+    "frt_kv_append_fp8",
     "frt_stream_attn_fp8_workspace_bytes", "frt_stream_attn_step_fp8", "frt_stream_step_fp8",
     "frt_decode_fp8_workspace_bytes", "frt_decode_attn_fp8", "frt_decode_step_fp8",
     "frt_status_str",
@@ -97,6 +98,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "frt_decode_workspace_bytes": (SZ, [RP, I32]),
         "frt_decode_attn": (I32, [RP, OP, MP, P, P, P, I32, ctypes.c_float, P, SZ, P, P, P]),
         "frt_decode_step": (I32, [RP, OP, MP, P, P, P, I32, ctypes.c_float, P, SZ, P, P, P]),
+        "frt_decode_step_noalloc": (I32, [RP, OP, MP, P, P, P, I32, ctypes.c_float, P, P, P]),
         "frt_kv_append_fp8": (I32, [RP, SP, OP, P, P, I32, P]),
         "frt_stream_attn_fp8_workspace_bytes": (SZ, [RP, I32, I32]),
         "frt_stream_attn_step_fp8": (I32, [RP, SP, OP, MP, P, P, P, I32, I32, ctypes.c_float, P,
@@ -308,6 +310,17 @@ def decode_step(ring: Ring, rope: Rope, msk: CMask, q, k_new, v_new, out, worksp
         ctypes.byref(cr), ctypes.byref(co), ctypes.byref(msk), _ptr(q), _ptr(k_new), _ptr(v_new),
         hq, softmax_scale, _ptr(workspace), workspace.numel() * workspace.element_size(),
         _ptr(out), _ptr(lse), _stream(stream)))
+
+
+def decode_step_noalloc(ring: Ring, rope: Rope, msk: CMask, q, k_new, v_new, out, lse=None,
+                        softmax_scale: float = 0.0, stream=None) -> None:
+    """frt_decode_step_noalloc: decode_step with the library's fixed device scratch
+    instead of a workspace (no allocation)."""
+    hq = q.shape[2]
+    cr, co = ring.c(), rope.c()
+    _check(load_library().frt_decode_step_noalloc(
+        ctypes.byref(cr), ctypes.byref(co), ctypes.byref(msk), _ptr(q), _ptr(k_new), _ptr(v_new),
+        hq, softmax_scale, _ptr(out), _ptr(lse), _stream(stream)))
 
 
 # ------------------------------------------------------------------ FP8 --

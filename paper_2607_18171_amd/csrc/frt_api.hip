@@ -802,6 +802,70 @@ frt_status frt_decode_step(const frt_ring *ring, const frt_rope *rope, const frt
                      workspace_bytes, out, lse, stream, true);
 }
 
+}  // extern "C"
+
+// ------------------------------------------- no-allocation decode step --
+// Device scratch of frt_decode_step_noalloc: file scope, one copy on every
+// GPU the library runs on, held until the process ends. Host code never
+// passes the array's name to a kernel (on the host it is a stand-in, not a
+// device address); it uses the address hipGetSymbolAddress returns for the
+// current device, looked up once per device.
+static __device__ __align__(256) unsigned char scratch[FRT_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch[kMaxDevices] = {};
+
+// This device's address of `scratch`, for a launch on `stream`.
+frt_status scratch_address(void *stream, void **out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0)
+    return fail(FRT_ERR_HIP, "hipGetDevice failed");
+  if (dev >= kMaxDevices) return fail(FRT_ERR_UNSUPPORTED, "device %d: at most %d devices", dev,
+                                      kMaxDevices);
+  if (stream != nullptr) {
+    hipDevice_t sdev = -1;
+    if (hipStreamGetDevice(static_cast<hipStream_t>(stream), &sdev) != hipSuccess)
+      return fail(FRT_ERR_HIP, "hipStreamGetDevice failed");
+    if (sdev != dev)
+      return fail(FRT_ERR_UNSUPPORTED, "the stream belongs to device %d but device %d is current",
+                  (int)sdev, dev);
+  }
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch[dev] == nullptr) {
+    void *ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || ptr == nullptr)
+      return fail(FRT_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d failed: %s", dev,
+                  hipGetErrorString(e));
+    g_scratch[dev] = ptr;
+  }
+  *out = g_scratch[dev];
+  return FRT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+frt_status frt_decode_step_noalloc(const frt_ring *ring, const frt_rope *rope,
+                                   const frt_mask *mask, const void *q, const void *k_new,
+                                   const void *v_new, int32_t num_q_heads, float softmax_scale,
+                                   void *out, float *lse, void *stream) {
+  const size_t need = frt_decode_workspace_bytes(ring, num_q_heads);
+  if (need > (size_t)FRT_NOALLOC_SCRATCH_BYTES)
+    return fail(FRT_ERR_WORKSPACE,
+                "decode needs %zu bytes of scratch; frt_decode_step_noalloc holds %zu",
+                need, (size_t)FRT_NOALLOC_SCRATCH_BYTES);
+  void *ws = nullptr;
+  frt_status s = scratch_address(stream, &ws);
+  if (s != FRT_OK) return s;
+  return decode_impl(ring, rope, mask, q, k_new, v_new, num_q_heads, softmax_scale, ws,
+                     (size_t)FRT_NOALLOC_SCRATCH_BYTES, out, lse, stream, true);
+}
+
 frt_status frt_timing_enable(int32_t on) {
   std::lock_guard<std::mutex> lk(g_tmu);
   g_timing = on != 0;

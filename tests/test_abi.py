@@ -30,7 +30,7 @@ def declared_symbols():
 def test_library_exports_every_declared_symbol():
     lib = frt.load_library()
     names = declared_symbols()
-    assert len(names) == 23
+    assert len(names) == 24
     for name in names:
         assert hasattr(lib, name), name
     assert sorted(B.EXPORTS) == names
