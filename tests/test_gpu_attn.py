@@ -19,6 +19,14 @@ from gpu_helpers import (to_dev, from_dev, bf16_dev_to_f64, build_rings, gpu_mas
 pytestmark = pytest.mark.gpu
 
 
+def lse_tol(wl):
+    """LSE tolerance (natural log): 2e-2 for unit-variance Q and K. The LSE moves by
+    the probability-weighted change of the scores, and the bf16 rounding of the
+    rotated query changes a score in proportion to its size, so the bound grows
+    with the logit scale (qk_scale^2: 3x for the 14B-like workload)."""
+    return 2e-2 * wl.qk_scale ** 2
+
+
 def run_step(case, ring, rope, with_lse=True):
     wl = case.wl
     q, k, v = to_dev(case.q), to_dev(case.k_new), to_dev(case.v_new)
@@ -70,7 +78,7 @@ def test_small_cases_all_rows(name, seed):
     out, lse = run_step(case, ring, rope)
     ref, ref_lse = oracle.stream_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask)
     check_close(bf16_dev_to_f64(out), ref, visible_vmax(oring, case), name)
-    assert np.abs(lse.cpu().numpy() - ref_lse).max() < 2e-2
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() < lse_tol(wl)
     # attention reads the ring, never writes it
     assert np.array_equal(from_dev(ring.k), oring.k)
 
@@ -85,24 +93,69 @@ def test_straddle_chunk_causal():
     check_close(bf16_dev_to_f64(out), ref, visible_vmax(oring, case), "straddle")
 
 
-def _sample_rows(wl, rng, extra):
-    rows = {0, wl.n - 1, wl.n // 2, 255, 256, 511}
-    rows |= set(int(x) for x in rng.integers(0, wl.n, extra))
-    return np.array(sorted(r for r in rows if 0 <= r < wl.n))
+# Full-size steps, computed once on the GPU and compared with the oracle head
+# group by head group (each group's oracle run takes seconds on the host).
+_FULL = {}
 
 
-@pytest.mark.parametrize("name", ["video_1p3b", "video_14b", "prefill_swa", "video_1p3b_pp4"])
-def test_full_size_sampled_rows(name):
-    wl = WORKLOADS[name]
+def _full_size(name, wl, lengths=None):
+    if name not in _FULL:
+        case = make_case(wl, 0, lengths=lengths)
+        ring, oring, rope = build_rings(case)
+        out, lse = run_step(case, ring, rope)
+        _FULL.clear()  # keep one workload's tensors at a time
+        _FULL[name] = (case, oring, bf16_dev_to_f64(out), lse.cpu().numpy(),
+                       visible_vmax(oring, case))
+    return _FULL[name]
+
+
+def _oracle_heads(case, oring, kv0, kv1, rows=None):
+    """The oracle's output and LSE for KV heads [kv0, kv1) and their query heads."""
+    G = case.wl.G
+    sub = oracle.RingState(oring.k[:, kv0:kv1], oring.v[:, kv0:kv1], oring.seq_len)
+    return oracle.stream_attn(sub, case.q[:, :, kv0 * G:kv1 * G], case.k_new[:, :, kv0:kv1],
+                              case.v_new[:, :, kv0:kv1], case.wl.rope, case.wl.mask, rows=rows)
+
+
+# (workload, stream lengths or None, KV heads per group)
+FULL = {
+    "video_1p3b": (WORKLOADS["video_1p3b"], None, 6),
+    "video_14b": (WORKLOADS["video_14b"], None, 8),
+    # the 14B-like step before its ring fills: steps 0 and 1 (4680 and 9360 keys)
+    "video_14b_step0": (shrink(WORKLOADS["video_14b"], prior_steps=0), None, 20),
+    "video_14b_step1": (shrink(WORKLOADS["video_14b"], prior_steps=1), None, 20),
+    "prefill_swa": (WORKLOADS["prefill_swa"], None, 8),
+}
+FULL_CASES = [(name, g) for name, (wl, _, per) in FULL.items() for g in range(wl.Hkv // per)]
+
+
+@pytest.mark.parametrize("name,group", FULL_CASES)
+def test_full_size_all_rows(name, group):
+    """Every output row of the full-size steps, one group of KV heads per case."""
+    wl, lengths, per = FULL[name]
+    case, oring, got, lse, vmax = _full_size(name, wl, lengths)
+    kv0, kv1 = group * per, (group + 1) * per
+    ref, ref_lse = _oracle_heads(case, oring, kv0, kv1)
+    G = wl.G
+    check_close(got[:, :, kv0 * G:kv1 * G], ref, vmax, "%s heads %d-%d" % (name, kv0, kv1))
+    assert np.abs(lse[:, kv0 * G:kv1 * G] - ref_lse).max() < lse_tol(wl)
+
+
+def test_full_size_sampled_rows_pp4():
+    """The four-cache step-pipeline layout: sampled rows of every head."""
+    wl = WORKLOADS["video_1p3b_pp4"]
     case = make_case(wl, 0)
     ring, oring, rope = build_rings(case)
     out, lse = run_step(case, ring, rope)
-    rows = _sample_rows(wl, np.random.default_rng(1), 24)
+    rng = np.random.default_rng(1)
+    rows = {0, wl.n - 1, wl.n // 2, 255, 256, 511}
+    rows |= set(int(x) for x in rng.integers(0, wl.n, 24))
+    rows = np.array(sorted(rows))
     ref, ref_lse = oracle.stream_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask,
                                       rows=rows)
     got = bf16_dev_to_f64(out)
-    check_close(got[:, rows], ref[:, rows], visible_vmax(oring, case), name)
-    assert np.abs(lse.cpu().numpy()[:, :, rows] - ref_lse[:, :, rows]).max() < 2e-2
+    check_close(got[:, rows], ref[:, rows], visible_vmax(oring, case), "pp4")
+    assert np.abs(lse.cpu().numpy()[:, :, rows] - ref_lse[:, :, rows]).max() < lse_tol(wl)
     assert np.all(np.isfinite(got))
 
 
@@ -114,7 +167,7 @@ def test_v_all_ones_gives_ones():
         v[:] = 0x3F80
     ring, oring, rope = build_rings(case)
     out, _ = run_step(case, ring, rope)
-    assert np.abs(bf16_dev_to_f64(out) - 1.0).max() <= 8e-3
+    assert np.abs(bf16_dev_to_f64(out) - 1.0).max() <= 4e-3
 
 
 def test_poisoned_invisible_slots_do_not_change_output():
@@ -213,7 +266,7 @@ def test_very_negative_first_tile():
     out, lse = run_step(case, ring, rope)
     ref, ref_lse = oracle.stream_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask)
     check_close(bf16_dev_to_f64(out), ref, visible_vmax(oring, case), "negative first tile")
-    assert np.abs(lse.cpu().numpy() - ref_lse).max() < 2e-2
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() < lse_tol(wl)
 
 
 @pytest.mark.parametrize("name,j", [("gqa_swa", 57), ("mha_causal", 20), ("gqa_d64", 64)])

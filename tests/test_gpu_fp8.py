@@ -311,3 +311,127 @@ def test_fp8_decode_rejects_head_dim_64():
     ring, oring, rope = build_fp8_rings(case, ks, vs)
     with pytest.raises(frt.FrtError):
         run_decode_fp8(wl, case, ring, rope)
+
+
+# ---- the FP8 step against exact attention (the fp64 oracle on the same inputs) ----
+from _helpers import FP8_MAX_REL_V, FP8_MEAN, e4m3_exact_case_values  # noqa: E402
+from gpu_helpers import visible_vmax, check_close, MAX_ERR_REL_V, MEAN_ERR  # noqa: E402
+
+EXACT_SMALL = dict(SMALL)
+# the 14B-like step's logit scale (Q and K drawn with std sqrt(3)) over a short window
+EXACT_SMALL["video_vpart_std3"] = shrink(SMALL["video_vpart"], qk_scale=float(np.sqrt(3.0)))
+
+
+def exact_oracle_ring(case):
+    wl = case.wl
+    oring = oracle.new_ring(wl.B, wl.Hkv, wl.C, wl.d)
+    for k, v in case.prior_steps:
+        oring = oracle.kv_append(oring, k, v, wl.rope)
+    for b, (k, v) in enumerate(case.prior_fills):
+        for s in range(0, k.shape[1], wl.C):
+            e = min(k.shape[1], s + wl.C)
+            oring = oracle.kv_append(oring, k[:, s:e], v[:, s:e], wl.rope, streams=[b])
+    return oring
+
+
+def check_fp8_vs_exact(got, ref, vmax, what):
+    err = np.abs(got - ref)
+    assert np.all(np.isfinite(got)), what
+    mx, mean = float(err.max()), float(err.mean())
+    print("%s vs exact: max|err| %.3g of max|V|, mean %.3g" % (what, mx / vmax, mean))
+    assert mx <= FP8_MAX_REL_V * vmax, "%s: max|err| %.3g of max|V|" % (what, mx / vmax)
+    assert mean <= FP8_MEAN, "%s: mean|err| %.3g" % (what, mean)
+
+
+@pytest.mark.parametrize("name", sorted(EXACT_SMALL))
+def test_fp8_attention_small_against_exact(name):
+    wl = EXACT_SMALL[name]
+    case = make_case(wl, 2)
+    ks, vs = scales(wl, 2)
+    ring, _, rope = build_fp8_rings(case, ks, vs)
+    out, _ = run_fp8_step(case, ring, rope)
+    oring = exact_oracle_ring(case)
+    ref, _ = oracle.stream_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask)
+    check_fp8_vs_exact(bf16_dev_to_f64(out), ref, visible_vmax(oring, case), name)
+
+
+@pytest.mark.parametrize("name", ["video_1p3b", "video_14b", "prefill_swa", "decode"])
+def test_fp8_full_size_against_exact(name):
+    wl = WORKLOADS[name]
+    case = make_case(wl, 0)
+    ks, vs = scales(wl, 0)
+    ring, _, rope = build_fp8_rings(case, ks, vs)
+    if wl.n == 1:
+        out, _ = run_decode_fp8(wl, case, ring, rope)
+        rows = np.array([0])
+    else:
+        out, _ = run_fp8_step(case, ring, rope)
+        rows = np.unique(np.linspace(0, wl.n - 1, 64).astype(np.int64))
+    oring = exact_oracle_ring(case)
+    ref, _ = oracle.stream_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask,
+                                rows=rows)
+    check_fp8_vs_exact(bf16_dev_to_f64(out)[:, rows], ref[:, rows], visible_vmax(oring, case),
+                       name)
+
+
+def test_fp8_equals_exact_attention_on_inputs_the_format_represents():
+    """No rotation, softmax scale ln 2 (base-2 scores equal q.k), scales 1, integer
+    queries and keys and quarter-integer values e4m3 represents, scores within 8 of
+    each row's maximum (so every weight is a normal e4m3 code): every operand and
+    weight the FP8 kernel codes is exact, so its result is exact attention up to
+    fp32 accumulation and the bf16 output rounding."""
+    wl = shrink(WORKLOADS["prefill_swa"], B=2, Hq=4, Hkv=2, n=70, C=192, rope=RopeSpec(0),
+                mask=MaskSpec(MASK_CAUSAL, 0, 150), len_lo=0, len_hi=400)
+    case = make_case(wl, 6, lengths=np.array([130, 300]))
+    rng = np.random.default_rng(7)
+    for i, (k, v) in enumerate(case.prior_fills):
+        case.prior_fills[i] = (e4m3_exact_case_values(rng, k.shape, -1, 1, 1),
+                               e4m3_exact_case_values(rng, v.shape, -4, 4, 0.25))
+    case.k_new[:] = e4m3_exact_case_values(rng, case.k_new.shape, -1, 1, 1)
+    case.v_new[:] = e4m3_exact_case_values(rng, case.v_new.shape, -4, 4, 0.25)
+    case.q[:] = 0
+    for b in range(wl.B):
+        for i in range(wl.n):
+            for h in range(wl.Hq):
+                dims = rng.choice(wl.d, 4, replace=False)
+                case.q[b, i, h, dims] = e4m3_exact_case_values(rng, 4, -1, 1, 2) | 0x3f80
+    ones = np.ones((wl.B, wl.Hkv), np.float32)
+    ring, oring8, rope = build_fp8_rings(case, ones, ones)
+    q, k, v = to_dev(case.q), to_dev(case.k_new), to_dev(case.v_new)
+    out = torch.empty_like(q)
+    ws = torch.empty(frt.stream_attn_fp8_workspace_bytes(ring, wl.n, wl.Hq), dtype=torch.uint8,
+                     device="cuda")
+    ln2 = float(np.float32(np.log(2.0)))
+    frt.stream_attn_step_fp8(ring, rope, gpu_mask(wl), q, k, v, out, ws, softmax_scale=ln2)
+    torch.cuda.synchronize()
+    oring = exact_oracle_ring(case)
+    ref, _ = oracle.stream_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask,
+                                scale=ln2)
+    got = bf16_dev_to_f64(out)
+    check_close(got, ref, visible_vmax(oring, case), "exact inputs")
+    # the rounding of the output to bf16 is the only error left
+    excess = np.abs(got - ref) - (np.abs(ref) * 2.0 ** -8 + 1e-6)
+    w = np.unravel_index(np.argmax(excess), excess.shape)
+    assert excess.max() <= 0, (w, got[w], ref[w])
+
+
+def test_fp8_very_negative_first_tile():
+    """Every row's first visible tile scores far below the row's later keys: the FP8
+    kernel's first raise of its reference max must not turn the empty accumulator
+    into 0 * inf."""
+    wl = shrink(WORKLOADS["prefill_swa"], B=1, Hq=2, Hkv=1, n=64, C=256, rope=RopeSpec(0),
+                mask=MaskSpec(MASK_CAUSAL, 0, 0))
+    case = make_case(wl, 9, lengths=np.array([160]))
+    case.q[:] = 0x4080  # 4.0
+    k0, _ = case.prior_fills[0]
+    k0[:, :64] = 0x4080 | 0x8000
+    k0[:, 64:] = draw_bf16(np.random.default_rng(3), k0[:, 64:].shape, 0.05)
+    case.k_new[:] = draw_bf16(np.random.default_rng(4), case.k_new.shape, 0.05)
+    ks = np.full((1, 1), 0.02, np.float32)
+    vs = np.full((1, 1), 0.02, np.float32)
+    ring, oring, rope = build_fp8_rings(case, ks, vs)
+    out, lse = run_fp8_step(case, ring, rope)
+    ref, ref_lse = fp8.stream_attn_fp8(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask,
+                                       ks, vs)
+    check_fp8(bf16_dev_to_f64(out), ref, vmax_fp8(oring, case, vs), "negative first tile")
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() < 2e-2

@@ -241,3 +241,133 @@ def test_spread_mass_stays_in_normal_codes():
     want = (w[:, None] * np.vstack([V, Vown])).sum(axis=0) / w.sum()
     assert np.allclose(out[0, 0, 0], want, rtol=0, atol=1e-12)
     assert abs(lse[0, 0, 0] - math.log(2.0 ** 12 + N + 1)) < 1e-9
+
+
+# ---- FP8 against exact attention ------------------------------------------
+from workloads import WORKLOADS, make_case, shrink  # noqa: E402
+from _helpers import FP8_MAX_REL_V, FP8_MEAN, e4m3_exact_case_values  # noqa: E402
+
+LN2 = math.log(2.0)
+
+
+def _both_rings(case, nh, ks, vs):
+    """The exact oracle's ring and the FP8 oracle's ring of the case's first nh KV
+    heads, filled with the same prior tokens."""
+    wl = case.wl
+    o = oracle.new_ring(wl.B, nh, wl.C, wl.d)
+    f = fp8.RingFP8(wl.B, nh, wl.C, wl.d)
+    for k, v in case.prior_steps:
+        o = oracle.kv_append(o, k[:, :, :nh], v[:, :, :nh], wl.rope)
+        fp8.kv_append_fp8(f, k[:, :, :nh], v[:, :, :nh], wl.rope, ks, vs)
+    for b, (k, v) in enumerate(case.prior_fills):
+        for s in range(0, k.shape[1], wl.C):
+            e = min(k.shape[1], s + wl.C)
+            o = oracle.kv_append(o, k[:, s:e, :nh], v[:, s:e, :nh], wl.rope, streams=[b])
+            fp8.kv_append_fp8(f, k[:, s:e, :nh], v[:, s:e, :nh], wl.rope, ks, vs, streams=[b])
+    return o, f
+
+
+def _visible_vmax(o, case, nh):
+    wl = case.wl
+    vals = [np.abs(oracle.bf16_to_f64(case.v_new[:, :, :nh])).max()]
+    for b in range(wl.B):
+        L = int(o.seq_len[b])
+        held = min(L, wl.C)
+        if held:
+            slots = oracle.slots_of_tokens(np.arange(L - held, L), wl.C)
+            vals.append(np.abs(oracle.bf16_to_f64(o.v[b][:, slots])).max())
+    return float(max(vals))
+
+
+@pytest.mark.parametrize("mask,G", [(MaskSpec(MASK_CAUSAL, 0, 0), 1),
+                                    (MaskSpec(MASK_CAUSAL, 0, 19), 3),
+                                    (MaskSpec(MASK_BLOCK_CAUSAL, 6, 2), 2)])
+def test_fp8_equals_exact_attention_on_inputs_the_format_represents(mask, G):
+    """With no rotation, softmax scale ln 2 (base-2 scores equal q.k), key and value
+    scales 1, integer queries and keys and quarter-integer values that e4m3
+    represents, and every row's scores within 16 of its maximum, each coded weight
+    2^(s - m + 7) is an exact e4m3 value: the FP8 step then has no rounding at all
+    and equals exact attention."""
+    rng = np.random.default_rng(40 + G)
+    B, Hkv, C, d, n = 2, 2, 24, 32, 6
+    Hq = Hkv * G
+    none = RopeSpec(ROPE_NONE)
+    ks = np.ones((B, Hkv), np.float32)
+    vs = np.ones((B, Hkv), np.float32)
+    o = oracle.new_ring(B, Hkv, C, d)
+    f = fp8.RingFP8(B, Hkv, C, d)
+    for step in (7, 8, 9):  # 24 tokens: the ring is full, slot 0 holds token 0
+        k = e4m3_exact_case_values(rng, (B, step, Hkv, d), -2, 2, 1)
+        v = e4m3_exact_case_values(rng, (B, step, Hkv, d), -4, 4, 0.25)
+        o = oracle.kv_append(o, k, v, none)
+        fp8.kv_append_fp8(f, k, v, none, ks, vs)
+    q = np.zeros((B, n, Hq, d), np.uint16)
+    # four nonzero entries of +-1 per query: every score lies in [-8, 8]
+    for b in range(B):
+        for i in range(n):
+            for h in range(Hq):
+                dims = rng.choice(d, 4, replace=False)
+                q[b, i, h, dims] = e4m3_exact_case_values(rng, 4, -1, 1, 2) | 0x3f80
+    k_new = e4m3_exact_case_values(rng, (B, n, Hkv, d), -2, 2, 1)
+    v_new = e4m3_exact_case_values(rng, (B, n, Hkv, d), -4, 4, 0.25)
+    ref, ref_lse = oracle.stream_attn(o, q, k_new, v_new, none, mask, scale=LN2)
+    got, lse = fp8.stream_attn_fp8(f, q, k_new, v_new, none, mask, ks, vs, scale=LN2)
+    assert np.abs(got - ref).max() <= 1e-12
+    assert np.abs(lse - ref_lse).max() <= 1e-12
+
+
+SMALL_FP8 = {
+    "video_small": shrink(WORKLOADS["video_1p3b"], Hq=2, Hkv=2, n=72, C=288,
+                          rope=RopeSpec(3, (44, 42, 42), (4, 6)),
+                          mask=MaskSpec(MASK_BLOCK_CAUSAL, 72, 4), prior_steps=6),
+    "video14_small": shrink(WORKLOADS["video_14b"], Hq=2, Hkv=2, n=72, C=432,
+                            rope=RopeSpec(3, (44, 42, 42), (4, 6)),
+                            mask=MaskSpec(MASK_BLOCK_CAUSAL, 72, 6), prior_steps=9),
+    "gqa_swa": shrink(WORKLOADS["prefill_swa"], B=3, Hq=8, Hkv=2, n=100, C=256,
+                      mask=MaskSpec(MASK_CAUSAL, 0, 200), len_lo=0, len_hi=800),
+    "mha_causal": shrink(WORKLOADS["prefill_swa"], B=2, Hq=4, Hkv=4, n=37, C=512,
+                         mask=MaskSpec(MASK_CAUSAL, 0, 0), len_lo=0, len_hi=400),
+}
+
+# (workload, KV heads evaluated, query rows evaluated or None for all)
+FULL_FP8 = {
+    "video_1p3b": (WORKLOADS["video_1p3b"], 2, np.unique(np.linspace(0, 4679, 512).astype(int))),
+    "video_14b": (WORKLOADS["video_14b"], 2, np.unique(np.linspace(0, 4679, 512).astype(int))),
+    "prefill_swa": (WORKLOADS["prefill_swa"], 1, None),
+    "decode": (WORKLOADS["decode"], 1, None),
+}
+
+
+def _fp8_vs_exact(wl, nh, rows, seed=0):
+    case = make_case(wl, seed)
+    ks = np.full((wl.B, nh), 0.02 * wl.qk_scale, np.float32)
+    vs = np.full((wl.B, nh), 0.02, np.float32)
+    o, f = _both_rings(case, nh, ks, vs)
+    q = case.q[:, :, :nh * wl.G]
+    kn, vn = case.k_new[:, :, :nh], case.v_new[:, :, :nh]
+    ref, _ = oracle.stream_attn(o, q, kn, vn, wl.rope, wl.mask, rows=rows)
+    got, _ = fp8.stream_attn_fp8(f, q, kn, vn, wl.rope, wl.mask, ks, vs, rows=rows)
+    sel = slice(None) if rows is None else rows
+    err = np.abs(got[:, sel] - ref[:, sel])
+    return float(err.max()), float(err.mean()), _visible_vmax(o, case, nh)
+
+
+@pytest.mark.parametrize("name", sorted(SMALL_FP8))
+def test_fp8_oracle_within_fp8_tolerance_of_exact_small(name):
+    wl = SMALL_FP8[name]
+    mx, mean, vmax = _fp8_vs_exact(wl, wl.Hkv, None)
+    assert mx <= FP8_MAX_REL_V * vmax and mean <= FP8_MEAN, (mx / vmax, mean)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", sorted(FULL_FP8))
+def test_fp8_oracle_within_fp8_tolerance_of_exact_full_size(name):
+    """The FP8 step's definition against exact attention on the full-size workloads
+    (a sample of heads and, for the video steps, 512 query rows spread over the
+    chunk). On the 14B-like step, whose logits have std 3, the coding of Q, K, V and
+    the weights in e4m3 costs about 1.2e-2 on average: twelve times the bf16 bound,
+    within the FP8 tolerance (32 times it)."""
+    wl, nh, rows = FULL_FP8[name]
+    mx, mean, vmax = _fp8_vs_exact(wl, nh, rows)
+    print("%s: max|err| %.3g of max|V|, mean %.3g" % (name, mx / vmax, mean))
+    assert mx <= FP8_MAX_REL_V * vmax and mean <= FP8_MEAN, (mx / vmax, mean)
