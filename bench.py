@@ -3,19 +3,24 @@
 A step is the whole hot path for one batch: frt_stream_step (chunk
 preparation, attention, and the append of the prepared chunk), or for the
 decode workload frt_decode_step (split + combine, the combine also appending
-the token).
+the token). The default workload is the 14B-like video step, the largest
+configuration of the video-step target that fits one GPU.
 Inputs are seeded synthetic bf16 tensors already resident in HBM; the ring is
 pre-filled through the library's own append so the measured steps see a
-wrapped ring.
+wrapped ring. With --rings R > 1 the steps rotate over R copies of the ring
+(separate buffers, same contents), so that the 256 MB Infinity Cache cannot
+serve a step's reads from the previous step; the decode workload does this by
+default (R = 3) and also reports the same steps on one ring ("hot").
 
 Prints one JSON line. `value` is attention TFLOP/s per step (algorithmic
 flops: 4*d per visible (query, key) pair, no credit for masked or padded
 work) or, for decode, HBM GB/s per step (each visible K/V byte once plus
 q/out), over K plain steps. `roofline` reports the dominant kernel against
-MI355X's published peaks, its duration taken with HIP events around each
-launch on the kernel's stream over K further steps (the events themselves
-lengthen a step, so they are kept out of the throughput region).
-`cpu_baseline` times the fp64 oracle on a bounded sample of the same step.
+MI355X's published peaks, its duration taken with HIP events on the kernel's
+own dispatch over K further steps (mean, and the 10th/50th/90th percentiles
+of the launches); the events themselves lengthen a step, so they are kept out
+of the throughput region. `cpu_baseline` times the fp64 oracle on a bounded
+sample of the same step.
 """
 from __future__ import annotations
 
@@ -147,7 +152,7 @@ def cpu_baseline(wl, case, seconds: float, fp8: bool = False):
     for L in case.prior_lengths:
         flops += int(visible_counts(wl, int(L))[rows].sum()) * 4 * wl.d * wl.Hq
     return {"value": flops * reps / dt / 1e12, "unit": "TFLOP/s", "cores": _blas_threads(),
-            "kind": "oracle",
+            "host_cores": len(os.sched_getaffinity(0)), "kind": "oracle",
             "sample": "first %d of %d query tokens per stream, all %d heads, %d call(s) "
                       "(%.2f GFLOP fp64 each, %.1f s)"
                       % (len(rows), wl.n, wl.Hq, reps, flops / 1e9, dt)}
@@ -180,7 +185,7 @@ def cpu_baseline_decode(wl, case, seconds: float, fp8: bool = False):
         reps += 1
     _, by = step_work(wl, case.prior_lengths, 1 if fp8 else 2)
     return {"value": by * reps / dt / 1e9, "unit": "GB/s", "cores": _blas_threads(),
-            "kind": "oracle",
+            "host_cores": len(os.sched_getaffinity(0)), "kind": "oracle",
             "sample": "whole step, all %d streams, %d repetitions (%.1f MB each, %.1f s)"
                       % (wl.B, reps, by / 1e6, dt)}
 
@@ -193,7 +198,8 @@ WARMUP_MS = 200
 # HBM traffic per launch of the dominant kernel, from rocprofv3 FETCH_SIZE and
 # WRITE_SIZE passes scaled by a plain-copy calibration; used only while the
 # library's machine code for the kernel is the code the counters were taken on.
-TRAFFIC_FILES = {("chunk_attn", "video_1p3b"): "profiles/chunk_attn_video_1p3b.txt",
+TRAFFIC_FILES = {("chunk_attn", "video_14b"): "profiles/chunk_attn_video_14b.txt",
+                 ("chunk_attn", "video_1p3b"): "profiles/chunk_attn_video_1p3b.txt",
                  ("decode_split", "decode"): "profiles/decode_split_decode.txt",
                  ("chunk_attn_fp8", "video_1p3b"): "profiles/chunk_attn_fp8_video_1p3b.txt",
                  ("decode_split_fp8", "decode"): "profiles/decode_split_fp8_decode.txt"}
@@ -278,7 +284,10 @@ def main(argv=None):
                     help="untimed warm-up steps (default: %d ms of steps, then 3 more; "
                          "after an idle spell the part takes 15-20 ms to reach its steady "
                          "clock)" % WARMUP_MS)
-    ap.add_argument("--workload", default="video_1p3b", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="video_14b", choices=sorted(WORKLOADS))
+    ap.add_argument("--rings", type=int, default=0,
+                    help="ring copies the steps rotate over (default: 3 for decode, whose "
+                         "ring would otherwise stay in the Infinity Cache; 1 otherwise)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target length of the oracle's timed CPU sample (0 = skip)")
@@ -338,10 +347,23 @@ def main(argv=None):
         for s in range(0, k.shape[1], wl.C):
             e = min(k.shape[1], s + wl.C)
             append(ring.view_stream(b), rope, to_dev(k[:, s:e]), to_dev(v[:, s:e]))
+    decode = wl.n == 1
+    nrings = args.rings if args.rings > 0 else (3 if decode else 1)
+    rings = [ring]
+    for _ in range(nrings - 1):  # same contents, separate buffers
+        if args.fp8:
+            copy = frt.RingFp8(wl.B, wl.Hkv, wl.d, wl.C, torch.from_numpy(ks),
+                               torch.from_numpy(vs))
+            copy.k.copy_(ring.k)
+            copy.v.copy_(ring.v)
+            copy.seq_len.copy_(ring.seq_len)
+        else:
+            copy = frt.Ring(wl.B, wl.Hkv, wl.d, wl.C, k=ring.k.clone(), v=ring.v.clone(),
+                            seq_len=ring.seq_len.clone())
+        rings.append(copy)
     q, kn, vn = to_dev(case.q), to_dev(case.k_new), to_dev(case.v_new)
     out = torch.empty_like(q)
     msk = frt.mask(wl.mask.kind, wl.mask.block, wl.mask.window)
-    decode = wl.n == 1
     if decode and args.fp8:
         ws = torch.empty(frt.decode_fp8_workspace_bytes(ring, wl.Hq), dtype=torch.uint8,
                          device=dev)
@@ -355,15 +377,16 @@ def main(argv=None):
                          device=dev)
     torch.cuda.synchronize()
 
-    def step():
+    def step(r=0):
+        rg = rings[r]
         if decode and args.fp8:
-            frt.decode_step_fp8(ring, rope, msk, q, kn, vn, out, ws)
+            frt.decode_step_fp8(rg, rope, msk, q, kn, vn, out, ws)
         elif decode:  # attention and the one-token append in one call
-            frt.decode_step(ring, rope, msk, q, kn, vn, out, ws)
+            frt.decode_step(rg, rope, msk, q, kn, vn, out, ws)
         elif args.fp8:
-            frt.stream_step_fp8(ring, rope, msk, q, kn, vn, out, ws)
+            frt.stream_step_fp8(rg, rope, msk, q, kn, vn, out, ws)
         else:
-            frt.stream_step(ring, rope, msk, q, kn, vn, out, ws)
+            frt.stream_step(rg, rope, msk, q, kn, vn, out, ws)
 
     warmup = 0
     if args.warmup >= 0:
@@ -375,42 +398,44 @@ def main(argv=None):
         # decode step appends one token per stream, so its warm-up runs the
         # attention alone and the stream lengths stay those of the workload;
         # the chunk steps see a window of the ring that is already full.
-        def warm():
+        def warm(r):
             if decode and args.fp8:
-                frt.decode_attn_fp8(ring, rope, msk, q, kn, vn, out, ws)
+                frt.decode_attn_fp8(rings[r], rope, msk, q, kn, vn, out, ws)
             elif decode:
-                frt.decode_attn(ring, rope, msk, q, kn, vn, out, ws)
+                frt.decode_attn(rings[r], rope, msk, q, kn, vn, out, ws)
             else:
-                step()
+                step(r)
         t0 = time.perf_counter()
         while warmup + 8 <= max_warm and time.perf_counter() - t0 < WARMUP_MS * 1e-3:
-            for _ in range(8):
-                warm()
+            for i in range(8):
+                warm((warmup + i) % nrings)
             warmup += 8
             torch.cuda.synchronize()
-        for _ in range(3):
-            step()
+        for i in range(3):
+            step(i % nrings)
         warmup += 3
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
 
-    def timed_steps():
-        """K steps between two events on the launch stream; returns (ms per
-        step, algorithmic flops per step, algorithmic bytes per step)."""
-        lengths = ring.seq_len.cpu().numpy().copy()
+    def timed_steps(nr):
+        """K steps rotating over the first nr rings, between two events on the
+        launch stream; returns (ms per step, algorithmic flops per step,
+        algorithmic bytes per step)."""
+        lengths = [rg.seq_len.cpu().numpy().copy() for rg in rings[:nr]]
         ev0 = torch.cuda.Event(enable_timing=True)
         ev1 = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         ev0.record(stream)
-        for _ in range(args.steps):
-            step()
+        for s in range(args.steps):
+            step(s % nr)
         ev1.record(stream)
         torch.cuda.synchronize()
-        # algorithmic work (lengths advance by n per step)
+        # algorithmic work (a ring's lengths advance by n each time it is used)
         flops = bytes_ = 0
         for s in range(args.steps):
-            f, by = step_work(wl, lengths + s * wl.n, 1 if args.fp8 else 2)
+            f, by = step_work(wl, lengths[s % nr], 1 if args.fp8 else 2)
+            lengths[s % nr] = lengths[s % nr] + wl.n
             flops += f
             bytes_ += by
         return ev0.elapsed_time(ev1) / args.steps, flops / args.steps, bytes_ / args.steps
@@ -418,18 +443,31 @@ def main(argv=None):
     # Throughput: K plain steps. Per-kernel durations: K more steps with the
     # library's per-launch events, which add a few microseconds around every
     # launch (a third of a decode step), so they stay out of the first region.
-    ms_step, flops_step, bytes_step = timed_steps()
+    ms_step, flops_step, bytes_step = timed_steps(nrings)
+    hot = None
+    if nrings > 1:  # the same steps on one ring, whose reads the Infinity Cache may serve
+        hms, hflops, hbytes = timed_steps(1)
+        hot = {"ms_per_step": hms,
+               "value": (hbytes / (hms * 1e-3) / 1e9) if decode else
+                        (hflops / (hms * 1e-3) / 1e12)}
     frt.timing_reset()
     frt.timing_enable(True)
-    _, kflops_step, kbytes_step = timed_steps()
+    _, kflops_step, kbytes_step = timed_steps(nrings)
     frt.timing_enable(False)
 
     kernels = {}
+    samples = {}
     for name in ("chunk_prep", "chunk_attn", "chunk_append", "decode_split", "decode_combine",
                  "rope_append", "seq_advance"):
         c, ms = frt.timing_query(name)
         if c:
             kernels[name] = {"launches": c, "avg_us": 1000.0 * ms / c}
+            samples[name] = np.array(frt.timing_samples(name)) * 1000.0
+
+    def pct(name):
+        p10, p50, p90 = np.percentile(samples[name], [10, 50, 90])
+        return {"p10_us": float(p10), "p50_us": float(p50), "p90_us": float(p90),
+                "avg_us": kernels[name]["avg_us"]}
 
     if decode:
         value = bytes_step / (ms_step * 1e-3) / 1e9
@@ -439,7 +477,8 @@ def main(argv=None):
         kname = "decode_split_fp8" if args.fp8 else "decode_split"
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": achieved / PEAK_HBM_GBS,
-                "traffic": recorded_traffic(kname, wl.name, frt.LIB_PATH), "kernel": kname}
+                "traffic": recorded_traffic(kname, wl.name, frt.LIB_PATH), "kernel": kname,
+                "step_frac": value / PEAK_HBM_GBS, "launch_us": pct("decode_split")}
     else:
         value = flops_step / (ms_step * 1e-3) / 1e12
         unit = "TFLOP/s"
@@ -449,7 +488,8 @@ def main(argv=None):
         kname = "chunk_attn_fp8" if args.fp8 else "chunk_attn"
         roof = {"bound": "mfma", "achieved": achieved, "peak": peak,
                 "unit": "TFLOP/s", "frac": achieved / peak,
-                "traffic": recorded_traffic(kname, wl.name, frt.LIB_PATH), "kernel": kname}
+                "traffic": recorded_traffic(kname, wl.name, frt.LIB_PATH), "kernel": kname,
+                "step_frac": value / peak, "launch_us": pct("chunk_attn")}
 
     cpu = None
     if args.cpu_seconds > 0 and not decode:
@@ -467,8 +507,9 @@ def main(argv=None):
                    "mask": "block_causal" if wl.mask.kind == MASK_BLOCK_CAUSAL else "causal",
                    "window": wl.mask.window, "seed": args.seed,
                    "step_gflop": flops_step / 1e9, "step_min_mb": bytes_step / 1e6,
-                   "parallelism": "single_gpu"},
+                   "rings": nrings, "parallelism": "single_gpu"},
         "kernels_us": {k: round(v["avg_us"], 2) for k, v in kernels.items()},
+        "hot": hot,
         "roofline": roof,
         "cpu_baseline": cpu,
     }
