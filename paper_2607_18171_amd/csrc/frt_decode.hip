@@ -3,10 +3,11 @@
 // Work. For stream b the query is token L = seq_len[b]; its visible ring
 // tokens [lo, L-1] are covered by n_b tiles of 32 tokens aligned to
 // multiples of 32 (token t lives in slot t mod C). Every (stream, KV head) is
-// cut into pieces of at most `per` consecutive tiles, `per` chosen from the
-// total so that the pieces spread evenly over the waves resident on the GPU
-// at once; wave k of the split pass streams piece k and writes its partial to
-// slot k. One more wave per (stream, KV head) writes the partial of the
+// cut into pc pieces of at most `per` tiles, `per` chosen from the total so
+// that the pieces spread evenly over the waves resident on the GPU at once;
+// piece j takes every pc-th tile from tile j, so that the waves of one head
+// read neighbouring memory at any moment. Wave k of the split pass streams
+// piece k and writes its partial to slot k. One more wave per (stream, KV head) writes the partial of the
 // step's own token.
 //
 // Split pass tiles stream straight from HBM into MFMA operand registers (no
@@ -160,9 +161,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecWavesPe
     // and per-stream values); stating it keeps its descriptors scalar and its
     // tile branches uniform: a descriptor the compiler takes for divergent
     // costs a readfirstlane loop per load.
+    // piece j of the head takes tiles j, j + pc, j + 2 pc, ... (at most per
+    // of them): the head's pieces stream neighbouring tiles at the same time
     const int kvh = uniform_i32((int)((wv - Kb) / pc));
-    const int j0 = uniform_i32((int)((wv - Kb) % pc) * per);
-    const int cnt = uniform_i32(min(st.n - j0, per));
+    const int j0 = uniform_i32((int)((wv - Kb) % pc));
+    const int cnt = uniform_i32((st.n - j0 + pc - 1) / pc);
     u32x4 kraw[kDecBufs][2][NKS];
     u32x4 vraw[kDecBufs][NDB];
     bf16x8 qf[NKS];
@@ -171,6 +174,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecWavesPe
                                                 (uint32_t)((size_t)C * D * 2));
     const __amdgpu_buffer_rsrc_t rv = make_rsrc(p.v_ring + head * (size_t)D * C,
                                                 (uint32_t)((size_t)D * C * 2));
+    const int tstride = kDecTile * pc;                       // tokens from one tile to the next
     const long long tk0 = st.T0 + (long long)kDecTile * j0;  // token of the first tile
     const int sb0 = (int)(tk0 % C);                           // its slot
     // visible tokens relative to tk0
@@ -181,10 +185,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecWavesPe
 
     // tile i of the piece: K rows (block kb, A-row rho = c16 -> token
     // 8*(rho/4) + 4*kb + rho%4 of the tile) and V rows (d = 16*db + c16,
-    // tokens 8*g4 .. +8, one 16-byte piece of the slot's V block). A piece spans at most C + 62 tokens, so
-    // sb0 + 32 i < 2C + 32: at most two wraps.
+    // tokens 8*g4 .. +8, one 16-byte piece of the slot's V block). The head's
+    // tiles span at most C + 62 tokens, so sb0 + tstride i < 2C + 32: at most
+    // two wraps.
     auto issue = [&](int i, int buf) __attribute__((always_inline)) {
-      int sb = sb0 + kDecTile * i;
+      int sb = sb0 + tstride * i;
       sb = sb >= C ? sb - C : sb;
       sb = sb >= C ? sb - C : sb;
 #pragma unroll
@@ -236,7 +241,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecWavesPe
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const int rel = kDecTile * i + 8 * g4 + 4 * kb + r;
+            const int rel = tstride * i + 8 * g4 + 4 * kb + r;
             if (rel < rlo || rel > rhi) sacc[kb][r] = kNegInf;
             mt = fmaxf(mt, sacc[kb][r]);
           }

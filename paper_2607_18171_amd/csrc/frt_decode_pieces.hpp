@@ -1,7 +1,8 @@
-// Piece mapping of the decode split passes (bf16 and FP8 rings): the visible
+// Piece sizing of the decode split passes (bf16 and FP8 rings): the visible
 // ring tokens of each (stream, KV head) as 32-token tiles, cut into pieces of
-// at most `per` consecutive tiles, one wave each. Templates over the pass's
-// parameter block (seq_len, mask, C, B, Hkv are all they read).
+// at most `per` tiles, one wave each (which tiles a piece takes is the
+// pass's choice). Templates over the pass's parameter block (seq_len, mask,
+// C, B, Hkv are all they read).
 #pragma once
 #include "frt_launch.hpp"
 
