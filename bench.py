@@ -20,7 +20,11 @@ MI355X's published peaks, its duration taken with HIP events on the kernel's
 own dispatch over K further steps (mean, and the 10th/50th/90th percentiles
 of the launches); the events themselves lengthen a step, so they are kept out
 of the throughput region. `cpu_baseline` times the fp64 oracle on a bounded
-sample of the same step.
+sample of the same step. `clock_power` is the graphics clock and socket power
+amd-smi reads while the attention repeats (the part runs at its power limit
+under this load, so the clock differs between parts), and `library` times the
+vendor libraries on the same part: torch's fused attention and a hipBLASLt
+GEMM, or for decode a device copy.
 """
 from __future__ import annotations
 
@@ -190,6 +194,113 @@ def cpu_baseline_decode(wl, case, seconds: float, fp8: bool = False):
                       % (wl.B, reps, by / 1e6, dt)}
 
 
+def clock_power(run, seconds: float = 1.5):
+    """Graphics clock and socket power while `run` (a few steps, synchronised)
+    repeats for about `seconds`, sampled with amd-smi: the part runs at its
+    power limit under this load, so the clock a kernel gets differs from one
+    MI355X to another. None where amd-smi is missing or prints nothing usable."""
+    import subprocess
+    import threading
+
+    samples = []
+    stop = threading.Event()
+
+    def sample():
+        while not stop.is_set():
+            try:
+                r = subprocess.run(["amd-smi", "metric", "-p", "-c", "--json"],
+                                   capture_output=True, text=True, timeout=10)
+                samples.append(json.loads(r.stdout))
+            except Exception:
+                pass
+            stop.wait(0.1)
+
+    th = threading.Thread(target=sample, daemon=True)
+    t0 = time.perf_counter()
+    th.start()
+    while time.perf_counter() - t0 < seconds:
+        run()
+    stop.set()
+    th.join(timeout=15)
+    clk, pw = [], []
+    for d in samples:
+        try:
+            g = d["gpu_data"][0] if isinstance(d, dict) else d[0]
+            c = [v["clk"]["value"] for k, v in g["clock"].items() if k.startswith("gfx_")
+                 and isinstance(v.get("clk"), dict) and isinstance(v["clk"].get("value"), (int, float))]
+            if c:
+                clk.append(float(np.mean(c)))
+            w = g["power"]["socket_power"]["value"]
+            if isinstance(w, (int, float)):
+                pw.append(float(w))
+        except (KeyError, IndexError, TypeError):
+            continue
+    if not clk and not pw:
+        return None
+    return {"gfx_mhz": float(np.median(clk)) if clk else None,
+            "socket_w": float(np.median(pw)) if pw else None, "samples": len(samples),
+            "source": "amd-smi metric -p -c, during %.1f s of further steps" % seconds}
+
+
+def library_baseline(wl, dev):
+    """The vendor libraries on the same part, as context for the roofline
+    fraction. Chunk steps: torch's scaled_dot_product_attention (its flash or
+    memory-efficient kernel, never the math path) at the step's shape with all
+    C + n keys visible and no mask (more flops than the step; its own rate),
+    and a hipBLASLt bf16 GEMM. Decode: a 1 GiB device copy, the part's
+    streaming rate. An entry the library rejects is reported as its error."""
+    import torch
+    import torch.nn.functional as F
+
+    def timed(fn, iters):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters * 1e-3
+
+    g = torch.Generator(device=dev).manual_seed(0)
+    res = {}
+    if wl.n == 1:
+        a = torch.empty(1 << 28, device=dev, dtype=torch.float32)  # 1 GiB
+        b = torch.empty_like(a)
+        t = timed(lambda: b.copy_(a), 10)
+        res["copy_1gib"] = {"us": t * 1e6, "GB/s": 2 * a.numel() * 4 / t / 1e9,
+                            "note": "read + write bytes"}
+        del a, b
+        return res
+    nk = wl.C + wl.n
+    q = torch.randn(wl.B, wl.Hq, wl.n, wl.d, device=dev, dtype=torch.bfloat16, generator=g)
+    k = torch.randn(wl.B, wl.Hq, nk, wl.d, device=dev, dtype=torch.bfloat16, generator=g)
+    v = torch.randn(wl.B, wl.Hq, nk, wl.d, device=dev, dtype=torch.bfloat16, generator=g)
+    fl = 4.0 * wl.B * wl.Hq * wl.n * nk * wl.d
+    backends = [torch.nn.attention.SDPBackend.FLASH_ATTENTION,
+                torch.nn.attention.SDPBackend.EFFICIENT_ATTENTION]
+    try:
+        with torch.nn.attention.sdpa_kernel(backends):
+            t = timed(lambda: F.scaled_dot_product_attention(q, k, v), 5)
+        res["sdpa"] = {"us": t * 1e6, "TFLOP/s": fl / t / 1e12,
+                       "shape": "q %s, k/v %s (K/V heads expanded to the query heads), "
+                                "no mask" % (list(q.shape), list(k.shape))}
+    except RuntimeError as e:
+        res["sdpa"] = {"error": str(e)[:200]}
+    del q, k, v
+    n = 8192
+    a = torch.randn(n, n, device=dev, dtype=torch.bfloat16, generator=g)
+    b = torch.randn(n, n, device=dev, dtype=torch.bfloat16, generator=g)
+    t = timed(lambda: a @ b, 10)
+    res["gemm_bf16_8192"] = {"us": t * 1e6, "TFLOP/s": 2.0 * n ** 3 / t / 1e12}
+    del a, b
+    torch.cuda.synchronize()
+    return res
+
+
 # Default warm-up length: after an idle spell the part needs 15-20 ms of load
 # to reach its steady clock (a 1.3B-like step measured 823 -> 745 -> 727 ->
 # 701 -> 682 -> 672 us in consecutive 5-step windows from a cold start).
@@ -294,6 +405,11 @@ def main(argv=None):
     ap.add_argument("--fp8", action="store_true",
                     help="the FP8 (e4m3fn) ring (head_dim 128): frt_stream_step_fp8, or "
                          "frt_decode_step_fp8 for the decode workload")
+    ap.add_argument("--no-library", action="store_true",
+                    help="skip the vendor-library comparison (torch SDPA, hipBLASLt GEMM or a "
+                         "device copy at the same part)")
+    ap.add_argument("--no-clock-power", action="store_true",
+                    help="skip sampling the clock and socket power with amd-smi")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized device buffer 3 times (known HBM traffic for "
                          "scaling FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -491,6 +607,23 @@ def main(argv=None):
                 "traffic": recorded_traffic(kname, wl.name, frt.LIB_PATH), "kernel": kname,
                 "step_frac": value / peak, "launch_us": pct("chunk_attn")}
 
+    cp = None
+    if not args.no_clock_power:
+        def few():  # attention without the append: the streams keep their lengths
+            for i in range(4):
+                rg = rings[i % nrings]
+                if decode and args.fp8:
+                    frt.decode_attn_fp8(rg, rope, msk, q, kn, vn, out, ws)
+                elif decode:
+                    frt.decode_attn(rg, rope, msk, q, kn, vn, out, ws)
+                elif args.fp8:
+                    frt.stream_attn_step_fp8(rg, rope, msk, q, kn, vn, out, ws)
+                else:
+                    frt.stream_attn_step(rg, rope, msk, q, kn, vn, out, ws)
+            torch.cuda.synchronize()
+        cp = clock_power(few)
+    lib = None if args.no_library else library_baseline(wl, dev)
+
     cpu = None
     if args.cpu_seconds > 0 and not decode:
         cpu = cpu_baseline(wl, case, args.cpu_seconds, fp8=args.fp8)
@@ -511,6 +644,8 @@ def main(argv=None):
         "kernels_us": {k: round(v["avg_us"], 2) for k, v in kernels.items()},
         "hot": hot,
         "roofline": roof,
+        "clock_power": cp,
+        "library": lib,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
