@@ -23,8 +23,10 @@ of the throughput region. `cpu_baseline` times the fp64 oracle on a bounded
 sample of the same step. `clock_power` is the graphics clock and socket power
 amd-smi reads while the attention repeats (the part runs at its power limit
 under this load, so the clock differs between parts), and `library` times the
-vendor libraries on the same part: torch's fused attention and a hipBLASLt
-GEMM, or for decode a device copy.
+vendor libraries and an MFMA-only probe on the same part: a 1 GiB device
+copy, and for the chunk steps torch's fused attention, a hipBLASLt GEMM and
+the probe; `roofline.measured_peak` puts the dominant kernel against the probe
+(chunk steps) or the copy (decode) at this part's clock.
 """
 from __future__ import annotations
 
@@ -195,7 +197,7 @@ def cpu_baseline_decode(wl, case, seconds: float, fp8: bool = False):
 
 
 def clock_power(run, seconds: float = 1.5):
-    """Graphics clock and socket power while `run` (a few steps, synchronised)
+    """Graphics clock and socket power while `run` (a few launches, synchronised)
     repeats for about `seconds`, sampled with amd-smi: the part runs at its
     power limit under this load, so the clock a kernel gets differs from one
     MI355X to another. None where amd-smi is missing or prints nothing usable."""
@@ -239,16 +241,17 @@ def clock_power(run, seconds: float = 1.5):
         return None
     return {"gfx_mhz": float(np.median(clk)) if clk else None,
             "socket_w": float(np.median(pw)) if pw else None, "samples": len(samples),
-            "source": "amd-smi metric -p -c, during %.1f s of further steps" % seconds}
+            "source": "amd-smi metric -p -c, during %.1f s of further launches" % seconds}
 
 
 def library_baseline(wl, dev):
     """The vendor libraries on the same part, as context for the roofline
-    fraction. Chunk steps: torch's scaled_dot_product_attention (its flash or
+    fraction: a 1 GiB device copy (the part's streaming rate) and, for the
+    chunk steps, torch's scaled_dot_product_attention (its flash or
     memory-efficient kernel, never the math path) at the step's shape with all
     C + n keys visible and no mask (more flops than the step; its own rate),
-    and a hipBLASLt bf16 GEMM. Decode: a 1 GiB device copy, the part's
-    streaming rate. An entry the library rejects is reported as its error."""
+    and a hipBLASLt bf16 GEMM. An entry the library rejects is reported as its
+    error."""
     import torch
     import torch.nn.functional as F
 
@@ -267,13 +270,13 @@ def library_baseline(wl, dev):
 
     g = torch.Generator(device=dev).manual_seed(0)
     res = {}
+    a = torch.empty(1 << 28, device=dev, dtype=torch.float32)  # 1 GiB
+    b = torch.empty_like(a)
+    t = timed(lambda: b.copy_(a), 10)
+    res["copy_1gib"] = {"us": t * 1e6, "GB/s": 2 * a.numel() * 4 / t / 1e9,
+                        "note": "read + write bytes"}
+    del a, b
     if wl.n == 1:
-        a = torch.empty(1 << 28, device=dev, dtype=torch.float32)  # 1 GiB
-        b = torch.empty_like(a)
-        t = timed(lambda: b.copy_(a), 10)
-        res["copy_1gib"] = {"us": t * 1e6, "GB/s": 2 * a.numel() * 4 / t / 1e9,
-                            "note": "read + write bytes"}
-        del a, b
         return res
     nk = wl.C + wl.n
     q = torch.randn(wl.B, wl.Hq, wl.n, wl.d, device=dev, dtype=torch.bfloat16, generator=g)
@@ -299,6 +302,72 @@ def library_baseline(wl, dev):
     del a, b
     torch.cuda.synchronize()
     return res
+
+
+def mfma_loop(dev, fp8: bool, no_clock: bool = False):
+    """The MFMA-only probe (libfrt_probe.so): random operands, 4 chains per
+    wave, one block of 8 waves per CU. Returns its TFLOP/s and launch time (and
+    the clock and power while it repeats), or the reason it could not run."""
+    import ctypes
+    import torch
+    from paper_2607_18171_amd.build import PROBE_LIB
+    if not os.path.exists(PROBE_LIB):
+        return {"error": "%s not built" % PROBE_LIB}
+    lib = ctypes.CDLL(PROBE_LIB)
+    fn = lib.frt_probe_mfma_fp8 if fp8 else lib.frt_probe_mfma_bf16
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    g = torch.Generator(device=dev).manual_seed(0)
+    nfrag = 2 * 4 * 64  # fragments: 16 bytes (bf16) or 32 bytes (FP8) each
+    if fp8:
+        frags = (torch.randn(nfrag * 32, device=dev, generator=g) * 4).to(torch.float8_e4m3fn)
+    else:
+        frags = torch.randn(nfrag * 8, device=dev, generator=g).to(torch.bfloat16)
+    blocks, iters = 256, 4096
+    out = torch.empty(blocks * 512, device=dev, dtype=torch.float32)
+    stream = torch.cuda.current_stream()
+
+    def run():
+        rc = fn(frags.data_ptr(), out.data_ptr(), blocks, iters, stream.cuda_stream)
+        if rc != 0:
+            raise RuntimeError("frt_probe_mfma: HIP error %d" % rc)
+
+    for _ in range(3):
+        run()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    reps = 10
+    e0.record(stream)
+    for _ in range(reps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) / reps * 1e-3
+    flops = blocks * 8 * 4 * iters * 32 * 32 * (64 if fp8 else 16) * 2
+
+    def burst():
+        for _ in range(10):
+            run()
+        torch.cuda.synchronize()
+
+    cp = None if no_clock else clock_power(burst, 1.0)
+    # the same loop on all-zero operands: no switching in the multipliers
+    frags.zero_()
+    for _ in range(3):
+        run()
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    tz = e0.elapsed_time(e1) / reps * 1e-3
+    return {"us": t * 1e6, "TFLOP/s": flops / t / 1e12, "clock_power": cp,
+            "zero_operands_TFLOP/s": flops / tz / 1e12,
+            "config": "%d blocks x 8 waves, 4 chains of %d MFMAs (32x32x%d %s) on random "
+                      "operands, no memory or vector work"
+                      % (blocks, iters, 64 if fp8 else 16, "e4m3" if fp8 else "bf16")}
 
 
 # Default warm-up length: after an idle spell the part needs 15-20 ms of load
@@ -623,6 +692,20 @@ def main(argv=None):
             torch.cuda.synchronize()
         cp = clock_power(few)
     lib = None if args.no_library else library_baseline(wl, dev)
+    # the measured ceiling beside the published one: the MFMA-only probe at
+    # this part's clock for the chunk steps, the device copy for decode
+    if not args.no_library:
+        if decode:
+            mp = lib["copy_1gib"]["GB/s"]
+            roof["measured_peak"] = {"value": mp, "unit": "GB/s", "frac": roof["achieved"] / mp,
+                                     "source": "library.copy_1gib"}
+        else:
+            lib["mfma_loop"] = mfma_loop(dev, args.fp8, args.no_clock_power)
+            if "TFLOP/s" in lib["mfma_loop"]:
+                mp = lib["mfma_loop"]["TFLOP/s"]
+                roof["measured_peak"] = {"value": mp, "unit": "TFLOP/s",
+                                         "frac": roof["achieved"] / mp,
+                                         "source": "library.mfma_loop"}
 
     cpu = None
     if args.cpu_seconds > 0 and not decode:
