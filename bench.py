@@ -157,11 +157,22 @@ def cpu_baseline(wl, case, seconds: float, fp8: bool = False):
     flops = 0
     for L in case.prior_lengths:
         flops += int(visible_counts(wl, int(L))[rows].sum()) * 4 * wl.d * wl.Hq
-    return {"value": flops * reps / dt / 1e12, "unit": "TFLOP/s", "cores": _blas_threads(),
-            "host_cores": len(os.sched_getaffinity(0)), "kind": "oracle",
-            "sample": "first %d of %d query tokens per stream, all %d heads, %d call(s) "
-                      "(%.2f GFLOP fp64 each, %.1f s)"
-                      % (len(rows), wl.n, wl.Hq, reps, flops / 1e9, dt)}
+    res = {"value": flops * reps / dt / 1e12, "unit": "TFLOP/s", "cores": _blas_threads(),
+           "host_cores": len(os.sched_getaffinity(0)), "kind": "oracle",
+           "sample": "first %d of %d query tokens per stream, all %d heads, %d call(s) "
+                     "(%.2f GFLOP fp64 each, %.1f s)"
+                     % (len(rows), wl.n, wl.Hq, reps, flops / 1e9, dt)}
+    if not fp8 and wl.B * wl.n * wl.Hq * wl.C * wl.d <= 1 << 20:
+        # the pure-Python loop twin of the oracle, on the whole step of a tiny workload
+        from oracle import brute
+        model = brute.ListRing(wl.B, wl.Hkv, wl.C, wl.d)
+        for k, v in case.prior_steps:
+            model.append(k.tolist(), v.tolist(), wl.rope)
+        q, kn, vn = case.q.tolist(), case.k_new.tolist(), case.v_new.tolist()
+        t0 = time.perf_counter()
+        brute.attend(model, q, kn, vn, wl.rope, wl.mask, wl.Hq)
+        res["brute_twin_ms"] = 1e3 * (time.perf_counter() - t0)
+    return res
 
 
 def cpu_baseline_decode(wl, case, seconds: float, fp8: bool = False):
