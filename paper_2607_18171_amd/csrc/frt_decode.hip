@@ -296,11 +296,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kDecWavesPe
 
 // Combine pass: one block of kCombineThreads threads per (stream, KV head).
 // Thread t owns the 4-float groups t, t + kCombineThreads, ... of the head's
-// G x D outputs (query g = group / (D/4)). The head's partials are its pieces
-// (their slot range is recorded in the own-token slot by the split pass) and
-// its own-token partial; they are merged online in groups of kCombineGroup,
-// whose (max, sum, outputs) loads are independent, so the pass waits on
-// memory once for the own-token slot and once per group.
+// G x D outputs (query g = group / (D/4)). The head's partials are its
+// own-token partial, which starts the merge, and its pieces (their slot range
+// is recorded in the own-token slot by the split pass), merged online in
+// groups of kCombineGroup whose (max, sum, outputs) loads are independent, so
+// the pass waits on memory once for the own-token slot and once per group.
 constexpr int kCombineThreads = 256;
 constexpr int kCombineGroup = 16;
 
@@ -331,57 +331,53 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeP
     gq[f] = live[f] ? idx / Q4 : 0;
     e4[f] = live[f] ? 4 * (idx % Q4) : 0;
   }
+  // the merge starts from the own token's partial: its max and sum (1) from
+  // the own-token slot, its output row v_new itself
   float M[F], lt[F];
   f32x4 acc[F];
 #pragma unroll
   for (int f = 0; f < F; ++f) {
-    M[f] = kNegInf;
-    lt[f] = 0.f;
-    acc[f] = f32x4{0.f, 0.f, 0.f, 0.f};
+    M[f] = own[gq[f]];
+    lt[f] = own[G + gq[f]];
+    const u32x2 w = *reinterpret_cast<const u32x2 *>(p.v_new + (size_t)head * D + e4[f]);
+    acc[f] = f32x4{bf16_bits_to_f32(w[0] & 0xffffu), bf16_bits_to_f32(w[0] >> 16),
+                   bf16_bits_to_f32(w[1] & 0xffffu), bf16_bits_to_f32(w[1] >> 16)};
   }
-  for (int c0 = 0; c0 <= np; c0 += kCombineGroup) {
+  // then the pieces, kCombineGroup at a time. A group's loads carry no
+  // branch, so that they are all in flight together: entries past the last
+  // piece read the last piece again (finite: every piece holds a visible
+  // key) and count with weight zero.
+  for (int c0 = 0; c0 < np; c0 += kCombineGroup) {
     float mv[kCombineGroup][F], lv[kCombineGroup][F];
     f32x4 ov[kCombineGroup][F];
 #pragma unroll
     for (int j = 0; j < kCombineGroup; ++j) {
-      const int c = c0 + j;
+      const int c = min(c0 + j, np - 1);
+      const float *pp = p.ws + (size_t)(K + c) * pstride;
 #pragma unroll
       for (int f = 0; f < F; ++f) {
-        mv[j][f] = kNegInf;
-        lv[j][f] = 0.f;
-        ov[j][f] = f32x4{0.f, 0.f, 0.f, 0.f};
-        if (c < np) {
-          const float *pp = p.ws + (size_t)(K + c) * pstride;
-          mv[j][f] = pp[gq[f]];
-          lv[j][f] = pp[G + gq[f]];
-          ov[j][f] = *reinterpret_cast<const f32x4 *>(pp + oo + gq[f] * D + e4[f]);
-        } else if (c == np) {
-          mv[j][f] = own[gq[f]];
-          lv[j][f] = own[G + gq[f]];
-          const u32x2 w = *reinterpret_cast<const u32x2 *>(p.v_new + (size_t)head * D + e4[f]);
-          ov[j][f] = f32x4{bf16_bits_to_f32(w[0] & 0xffffu), bf16_bits_to_f32(w[0] >> 16),
-                           bf16_bits_to_f32(w[1] & 0xffffu), bf16_bits_to_f32(w[1] >> 16)};
-        }
+        mv[j][f] = pp[gq[f]];
+        lv[j][f] = pp[G + gq[f]];
+        ov[j][f] = *reinterpret_cast<const f32x4 *>(pp + oo + gq[f] * D + e4[f]);
       }
     }
 #pragma unroll
     for (int f = 0; f < F; ++f) {
-      // live partials have a positive sum (the own token's always has)
+      // every piece has a positive sum; the running state already has one
       float Mg = M[f];
 #pragma unroll
-      for (int j = 0; j < kCombineGroup; ++j) Mg = lv[j][f] > 0.f ? fmaxf(Mg, mv[j][f]) : Mg;
-      if (Mg != kNegInf) {
-        const float a = __builtin_amdgcn_exp2f(M[f] - Mg);  // M = -inf gives 0
-        acc[f] *= a;
-        lt[f] *= a;
+      for (int j = 0; j < kCombineGroup; ++j)
+        if (c0 + j < np) Mg = fmaxf(Mg, mv[j][f]);
+      const float a = __builtin_amdgcn_exp2f(M[f] - Mg);
+      acc[f] *= a;
+      lt[f] *= a;
 #pragma unroll
-        for (int j = 0; j < kCombineGroup; ++j) {
-          const float w = lv[j][f] > 0.f ? __builtin_amdgcn_exp2f(mv[j][f] - Mg) : 0.f;
-          acc[f] += ov[j][f] * w;
-          lt[f] += lv[j][f] * w;
-        }
-        M[f] = Mg;
+      for (int j = 0; j < kCombineGroup; ++j) {
+        const float w = c0 + j < np ? __builtin_amdgcn_exp2f(mv[j][f] - Mg) : 0.f;
+        acc[f] += ov[j][f] * w;
+        lt[f] += lv[j][f] * w;
       }
+      M[f] = Mg;
     }
   }
 #pragma unroll
