@@ -19,14 +19,16 @@ q/out), over K plain steps. `roofline` reports the dominant kernel against
 MI355X's published peaks, its duration taken with HIP events on the kernel's
 own dispatch over K further steps (mean, and the 10th/50th/90th percentiles
 of the launches); the events themselves lengthen a step, so they are kept out
-of the throughput region. `cpu_baseline` times the fp64 oracle on a bounded
-sample of the same step. `clock_power` is the graphics clock and socket power
-amd-smi reads while the attention repeats (the part runs at its power limit
-under this load, so the clock differs between parts), and `library` times the
-vendor libraries and an MFMA-only probe on the same part: a 1 GiB device
-copy, and for the chunk steps torch's fused attention, a hipBLASLt GEMM and
-the probe; `roofline.measured_peak` puts the dominant kernel against the probe
-(chunk steps) or the copy (decode) at this part's clock.
+of the throughput region. With --graph, `graph` times the same steps
+replayed from one HIP graph (no host launch cost between them).
+`cpu_baseline` times the fp64 oracle on a bounded sample of the same step. `clock_power` is the graphics
+clock and socket power amd-smi reads while the attention repeats (the part
+runs at its power limit under this load, so the clock differs between
+parts), and `library` times the vendor libraries and an MFMA-only probe on
+the same part: a 1 GiB device copy, and for the chunk steps torch's fused
+attention, a hipBLASLt GEMM and the probe; `roofline.measured_peak` puts the
+dominant kernel against the probe (chunk steps) or the copy (decode) at this
+part's clock.
 """
 from __future__ import annotations
 
@@ -488,6 +490,8 @@ def main(argv=None):
     ap.add_argument("--no-library", action="store_true",
                     help="skip the vendor-library comparison (torch SDPA, hipBLASLt GEMM or a "
                          "device copy at the same part)")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the same steps replayed from a HIP graph")
     ap.add_argument("--no-clock-power", action="store_true",
                     help="skip sampling the clock and socket power with amd-smi")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -526,7 +530,8 @@ def main(argv=None):
 
     # at most this many warm-up steps (the rotary table covers every position)
     max_warm = args.warmup if args.warmup >= 0 else (4000 if wl.n == 1 else 400)
-    total_steps = max_warm + 3 + 2 * args.steps  # warmup, plain pass, instrumented pass
+    # warm-up, plain, one-ring, instrumented and graph-replayed passes
+    total_steps = max_warm + 3 + 4 * args.steps
     max_tokens = int(case.prior_lengths.max()) + (total_steps + 1) * wl.n + 1
     rope = frt.Rope.for_tokens(wl.rope.mode, wl.rope.axis_dims, wl.rope.frame_hw, max_tokens,
                                wl.rope.base)
@@ -651,6 +656,41 @@ def main(argv=None):
     _, kflops_step, kbytes_step = timed_steps(nrings)
     frt.timing_enable(False)
 
+    graph = None
+    if args.graph:
+        # The same steps replayed from one HIP graph that holds a step per ring:
+        # no host launch cost between steps (what a serving loop that captures
+        # its step sees). Not the headline figure.
+        lengths = [rg.seq_len.cpu().numpy().copy() for rg in rings]
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for r in range(nrings):
+                step(r)
+        reps = max(1, args.steps // nrings)
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(reps):
+            g.replay()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        gms = ev0.elapsed_time(ev1) / (reps * nrings)
+        gf = gb = 0
+        for _ in range(reps):
+            for r in range(nrings):
+                f, by = step_work(wl, lengths[r], 1 if args.fp8 else 2)
+                lengths[r] = lengths[r] + wl.n
+                gf += f
+                gb += by
+        gf /= reps * nrings
+        gb /= reps * nrings
+        graph = {"ms_per_step": gms,
+                 "value": (gb / (gms * 1e-3) / 1e9) if decode else (gf / (gms * 1e-3) / 1e12),
+                 "steps": reps * nrings}
+        del g
+
     kernels = {}
     samples = {}
     for name in ("chunk_prep", "chunk_attn", "chunk_append", "decode_split", "decode_combine",
@@ -737,6 +777,7 @@ def main(argv=None):
                    "rings": nrings, "parallelism": "single_gpu"},
         "kernels_us": {k: round(v["avg_us"], 2) for k, v in kernels.items()},
         "hot": hot,
+        "graph": graph,
         "roofline": roof,
         "clock_power": cp,
         "library": lib,
