@@ -28,7 +28,9 @@ parts), and `library` times the vendor libraries and an MFMA-only probe on
 the same part: a 1 GiB device copy, and for the chunk steps torch's fused
 attention, a hipBLASLt GEMM and the probe; `roofline.measured_peak` puts the
 dominant kernel against the probe (chunk steps) or the copy (decode) at this
-part's clock.
+part's clock. Run without --workload, the line also carries
+`other_workloads`: the same steps of every other workload (bf16 and FP8),
+each measured briefly without the library, clock and CPU legs.
 """
 from __future__ import annotations
 
@@ -46,6 +48,7 @@ if ROOT not in sys.path:
 
 from workloads import WORKLOADS, make_case, MASK_BLOCK_CAUSAL, MASK_CAUSAL  # noqa: E402
 
+DEFAULT_WORKLOAD = "video_14b"
 METRIC = "attention TFLOP/s + % bf16 MFMA peak per streaming step; decode HBM GB/s"
 PEAK_BF16_TFLOPS = 2516.6   # MI355X dense bf16 MFMA (published 2.5 PFLOP/s)
 PEAK_FP8_TFLOPS = 5033.2    # MI355X dense fp8 MFMA (published 5.0 PFLOP/s)
@@ -469,57 +472,13 @@ def recorded_traffic(kernel: str, workload: str, lib_path: str):
     return int(fields["traffic_bytes_per_launch"])
 
 
-def main(argv=None):
-    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=-1,
-                    help="untimed warm-up steps (default: %d ms of steps, then 3 more; "
-                         "after an idle spell the part takes 15-20 ms to reach its steady "
-                         "clock)" % WARMUP_MS)
-    ap.add_argument("--workload", default="video_14b", choices=sorted(WORKLOADS))
-    ap.add_argument("--rings", type=int, default=0,
-                    help="ring copies the steps rotate over (default: 3 for decode, whose "
-                         "ring would otherwise stay in the Infinity Cache; 1 otherwise)")
-    ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-seconds", type=float, default=15.0,
-                    help="target length of the oracle's timed CPU sample (0 = skip)")
-    ap.add_argument("--fp8", action="store_true",
-                    help="the FP8 (e4m3fn) ring (head_dim 128): frt_stream_step_fp8, or "
-                         "frt_decode_step_fp8 for the decode workload")
-    ap.add_argument("--no-library", action="store_true",
-                    help="skip the vendor-library comparison (torch SDPA, hipBLASLt GEMM or a "
-                         "device copy at the same part)")
-    ap.add_argument("--graph", action="store_true",
-                    help="also time the same steps replayed from a HIP graph")
-    ap.add_argument("--no-clock-power", action="store_true",
-                    help="skip sampling the clock and socket power with amd-smi")
-    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
-                    help="only copy a MIB-sized device buffer 3 times (known HBM traffic for "
-                         "scaling FETCH_SIZE / WRITE_SIZE counters) and exit")
-    args = ap.parse_args(argv)
-    if args.copy_calibration:
-        import torch
-        a = torch.ones(args.copy_calibration << 18, dtype=torch.float32, device="cuda")
-        b = torch.empty_like(a)
-        for _ in range(3):
-            b.copy_(a)
-        torch.cuda.synchronize()
-        print(json.dumps({"copy_bytes_per_launch": a.numel() * 4}))
-        return 0
-
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the step runs on one MI355X and nothing in this "
-              "library crosses GPUs (requested --gpus %d)" % args.gpus, file=sys.stderr)
-        return 2
-
+def measure(args) -> dict:
+    """Measure one workload as `args` describes it; returns the JSON line's
+    fields."""
     import torch
     import paper_2607_18171_amd as frt
 
     wl = WORKLOADS[args.workload]
-    if args.fp8 and wl.d != 128:
-        print("--fp8 covers the workloads with head_dim 128", file=sys.stderr)
-        return 2
     case = make_case(wl, args.seed)
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
@@ -783,6 +742,93 @@ def main(argv=None):
         "library": lib,
         "cpu_baseline": cpu,
     }
+    return line
+
+
+# Measured after the default workload, each briefly (no library, clock or
+# CPU legs), so that one bench line holds every configuration:
+# (workload, FP8 ring)
+OTHER_WORKLOADS = (("video_1p3b", False), ("prefill_swa", False), ("decode", False),
+                   ("video_1p3b", True), ("decode", True))
+
+
+def summary(line: dict) -> dict:
+    """The compact record of one workload's measurement."""
+    r = line["roofline"]
+    return {"workload": line["config"]["workload"], "dtype": line["dtype"],
+            "ms_per_step": line["ms_per_step"], "value": line["value"],
+            "unit": line["unit"], "rings": line["config"]["rings"],
+            "kernel": r["kernel"], "kernel_us": r["launch_us"]["avg_us"],
+            "achieved": r["achieved"], "peak": r["peak"], "frac": r["frac"],
+            "step_frac": r["step_frac"], "kernels_us": line["kernels_us"],
+            "hot": line["hot"]}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=-1,
+                    help="untimed warm-up steps (default: %d ms of steps, then 3 more; "
+                         "after an idle spell the part takes 15-20 ms to reach its steady "
+                         "clock)" % WARMUP_MS)
+    ap.add_argument("--workload", default=None, choices=sorted(WORKLOADS),
+                    help="default %s; with no --workload the line also carries a brief "
+                         "measurement of every other workload (other_workloads)"
+                         % DEFAULT_WORKLOAD)
+    ap.add_argument("--rings", type=int, default=0,
+                    help="ring copies the steps rotate over (default: 3 for decode, whose "
+                         "ring would otherwise stay in the Infinity Cache; 1 otherwise)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target length of the oracle's timed CPU sample (0 = skip)")
+    ap.add_argument("--fp8", action="store_true",
+                    help="the FP8 (e4m3fn) ring (head_dim 128): frt_stream_step_fp8, or "
+                         "frt_decode_step_fp8 for the decode workload")
+    ap.add_argument("--no-library", action="store_true",
+                    help="skip the vendor-library comparison (torch SDPA, hipBLASLt GEMM or a "
+                         "device copy at the same part)")
+    ap.add_argument("--no-others", action="store_true",
+                    help="skip the brief measurement of the other workloads that a run "
+                         "without --workload adds")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the same steps replayed from a HIP graph")
+    ap.add_argument("--no-clock-power", action="store_true",
+                    help="skip sampling the clock and socket power with amd-smi")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only copy a MIB-sized device buffer 3 times (known HBM traffic for "
+                         "scaling FETCH_SIZE / WRITE_SIZE counters) and exit")
+    args = ap.parse_args(argv)
+    if args.copy_calibration:
+        import torch
+        a = torch.ones(args.copy_calibration << 18, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_per_launch": a.numel() * 4}))
+        return 0
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the step runs on one MI355X and nothing in this "
+              "library crosses GPUs (requested --gpus %d)" % args.gpus, file=sys.stderr)
+        return 2
+
+    explicit = args.workload is not None
+    if not explicit:
+        args.workload = DEFAULT_WORKLOAD
+    if args.fp8 and WORKLOADS[args.workload].d != 128:
+        print("--fp8 covers the workloads with head_dim 128", file=sys.stderr)
+        return 2
+    line = measure(args)
+    if not explicit and not args.no_others and not args.fp8:
+        others = []
+        for name, fp8 in OTHER_WORKLOADS:
+            sub = argparse.Namespace(**vars(args))
+            sub.workload, sub.fp8, sub.rings = name, fp8, 0
+            sub.cpu_seconds, sub.no_library, sub.no_clock_power, sub.graph = 0, True, True, False
+            others.append(summary(measure(sub)))
+        line["other_workloads"] = others
     print(json.dumps(line), flush=True)
     return 0
 
