@@ -164,3 +164,30 @@ def test_decode_split_count_independence():
         check_close(got, ref, visible_vmax(oring, case), "B%d" % B)
         assert np.abs(lse.cpu().numpy()[:1] - ref_lse).max() < 2e-2
     assert len(splits) == 3, splits
+
+
+@pytest.mark.parametrize("B", [65, 130])
+def test_decode_more_than_64_streams(B):
+    """The decode pass finds each wave's stream and piece range with wave-wide
+    scans over groups of 64 streams: batches past one and two groups, with
+    lengths from empty to a full ring, against the oracle; then the fused step's
+    ring and lengths against the oracle's."""
+    wl = shrink(WORKLOADS["decode"], B=B, Hq=4, Hkv=2, C=256,
+                mask=MaskSpec(MASK_CAUSAL, 0, 0))
+    rng = np.random.default_rng(B)
+    lengths = rng.integers(0, 256, B)
+    lengths[0], lengths[-1], lengths[B // 2] = 0, 255, 1
+    case = make_case(wl, B, lengths=lengths)
+    ring, oring, rope = build_rings(case, extra_tokens=2)
+    out, lse = run_decode(case, ring, rope)
+    ref, ref_lse = oracle.decode_attn(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask)
+    check_close(bf16_dev_to_f64(out), ref, visible_vmax(oring, case), "B%d" % B)
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() < 2e-2
+    ws = torch.empty(frt.decode_workspace_bytes(ring, wl.Hq), dtype=torch.uint8, device="cuda")
+    step_out = torch.empty_like(out)
+    frt.decode_step(ring, rope, gpu_mask(wl), to_dev(case.q), to_dev(case.k_new),
+                    to_dev(case.v_new), step_out, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(step_out.view(torch.int16), out.view(torch.int16))
+    oring = oracle.kv_append(oring, case.k_new, case.v_new, wl.rope)
+    assert ring_bytes_equal(ring, oring)

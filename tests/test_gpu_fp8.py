@@ -227,6 +227,9 @@ DECODE = {
     "g16": (shrink(WORKLOADS["decode"], B=2, Hq=32, Hkv=2, C=328), [327, 40]),
     "block_causal": (shrink(WORKLOADS["decode"], B=2, Hq=8, Hkv=2, C=512,
                             mask=MaskSpec(MASK_BLOCK_CAUSAL, 128, 2)), [300, 511]),
+    # more streams than one 64-lane scan group (twice over), empty to full rings
+    "streams_130": (shrink(WORKLOADS["decode"], B=130, Hq=4, Hkv=2, C=256),
+                    [0, 255, 1] + [(37 * b + 5) % 256 for b in range(3, 130)]),
 }
 
 
