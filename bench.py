@@ -24,11 +24,11 @@ replayed from one HIP graph (no host launch cost between them).
 `cpu_baseline` times the fp64 oracle on a bounded sample of the same step. `clock_power` is the graphics
 clock and socket power amd-smi reads while the attention repeats (the part
 runs at its power limit under this load, so the clock differs between
-parts), and `library` times the vendor libraries and an MFMA-only probe on
-the same part: a 1 GiB device copy, and for the chunk steps torch's fused
-attention, a hipBLASLt GEMM and the probe; `roofline.measured_peak` puts the
-dominant kernel against the probe (chunk steps) or the copy (decode) at this
-part's clock. Run without --workload, the line also carries
+parts), and `library` times the vendor libraries and two probes on the same
+part: a 1 GiB device copy; for the chunk steps torch's fused attention, a
+hipBLASLt GEMM and an MFMA-only probe; for decode a streaming-read probe of
+the split pass's bytes. `roofline.measured_peak` puts the dominant kernel
+against the probe of its kind at this part's clock. Run without --workload, the line also carries
 `other_workloads`: the same steps of every other workload (bf16 and FP8),
 each measured briefly without the library, clock and CPU legs.
 """
@@ -262,7 +262,7 @@ def clock_power(run, seconds: float = 1.5):
 
 def library_baseline(wl, dev):
     """The vendor libraries on the same part, as context for the roofline
-    fraction: a 1 GiB device copy (the part's streaming rate) and, for the
+    fraction: a 1 GiB device copy (read plus write) and, for the
     chunk steps, torch's scaled_dot_product_attention (its flash or
     memory-efficient kernel, never the math path) at the step's shape with all
     C + n keys visible and no mask (more flops than the step; its own rate),
@@ -384,6 +384,61 @@ def mfma_loop(dev, fp8: bool, no_clock: bool = False):
             "config": "%d blocks x 8 waves, 4 chains of %d MFMAs (32x32x%d %s) on random "
                       "operands, no memory or vector work"
                       % (blocks, iters, 64 if fp8 else 16, "e4m3" if fp8 else "bf16")}
+
+
+def stream_read(dev, nbytes: int):
+    """The streaming-read probe (libfrt_probe.so) on `nbytes`, the dominant
+    kernel's algorithmic bytes per launch: plain 16-byte loads over three
+    buffers of that size taken in turn (the same rotation as the cold decode
+    rings, so the Infinity Cache cannot serve a repeat), at a few grid sizes
+    and loads-in-flight counts; the best is the read rate this part reaches
+    for that many bytes in one launch."""
+    import ctypes
+    import torch
+    from paper_2607_18171_amd.build import PROBE_LIB
+    if not os.path.exists(PROBE_LIB):
+        return {"error": "%s not built" % PROBE_LIB}
+    lib = ctypes.CDLL(PROBE_LIB)
+    fn = lib.frt_probe_read
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                   ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    n = (nbytes + 15) // 16 * 16
+    g = torch.Generator(device=dev).manual_seed(0)
+    bufs = [torch.randint(0, 1 << 62, (n // 8,), device=dev, dtype=torch.int64, generator=g)
+            for _ in range(3)]
+    # grid-stride grids, and grids in which every thread issues all of its
+    # loads at once (one pass, blocks = words / (256 * unroll))
+    configs = [(blocks, unroll) for blocks in (2048, 4096, 8192, 16384) for unroll in (8, 16)]
+    configs += [(-(-n // (16 * 256 * unroll)), unroll) for unroll in (2, 4, 8)]
+    sink = torch.zeros(max(b for b, _ in configs), device=dev, dtype=torch.int32)
+    stream = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    table = {}
+    for blocks, unroll in configs:
+        def run(i):
+            rc = fn(bufs[i % 3].data_ptr(), n, sink.data_ptr(), blocks, unroll, stream.cuda_stream)
+            if rc != 0:
+                raise RuntimeError("frt_probe_read: HIP error %d" % rc)
+        for i in range(6):
+            run(i)
+        torch.cuda.synchronize()
+        reps = 30
+        e0.record(stream)
+        for i in range(reps):
+            run(i)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / reps * 1e-3
+        table["%dx%d" % (blocks, unroll)] = n / t / 1e9
+    best = max(table, key=table.get)
+    del bufs
+    torch.cuda.synchronize()
+    return {"GB/s": table[best], "us": n / table[best] / 1e3, "bytes": n,
+            "config": "%s blocks x loads in flight per thread, 256 threads a block, three "
+                      "buffers in turn" % best,
+            "by_config_GB/s": {k: round(v, 1) for k, v in table.items()}}
 
 
 # Default warm-up length: after an idle spell the part needs 15-20 ms of load
@@ -702,13 +757,17 @@ def measure(args) -> dict:
             torch.cuda.synchronize()
         cp = clock_power(few)
     lib = None if args.no_library else library_baseline(wl, dev)
-    # the measured ceiling beside the published one: the MFMA-only probe at
-    # this part's clock for the chunk steps, the device copy for decode
+    # the measured ceiling beside the published one, at this part's clock:
+    # the MFMA-only probe for the chunk steps, the streaming-read probe of the
+    # split pass's bytes for decode
     if not args.no_library:
         if decode:
-            mp = lib["copy_1gib"]["GB/s"]
-            roof["measured_peak"] = {"value": mp, "unit": "GB/s", "frac": roof["achieved"] / mp,
-                                     "source": "library.copy_1gib"}
+            lib["stream_read"] = stream_read(dev, int(kbytes_step))
+            if "GB/s" in lib["stream_read"]:
+                mp = lib["stream_read"]["GB/s"]
+                roof["measured_peak"] = {"value": mp, "unit": "GB/s",
+                                         "frac": roof["achieved"] / mp,
+                                         "source": "library.stream_read"}
         else:
             lib["mfma_loop"] = mfma_loop(dev, args.fp8, args.no_clock_power)
             if "TFLOP/s" in lib["mfma_loop"]:
@@ -786,8 +845,9 @@ def main(argv=None):
                     help="the FP8 (e4m3fn) ring (head_dim 128): frt_stream_step_fp8, or "
                          "frt_decode_step_fp8 for the decode workload")
     ap.add_argument("--no-library", action="store_true",
-                    help="skip the vendor-library comparison (torch SDPA, hipBLASLt GEMM or a "
-                         "device copy at the same part)")
+                    help="skip the vendor-library and probe comparison (a device copy; torch "
+                         "SDPA, hipBLASLt GEMM and the MFMA probe, or the streaming-read probe "
+                         "for decode)")
     ap.add_argument("--no-others", action="store_true",
                     help="skip the brief measurement of the other workloads that a run "
                          "without --workload adds")

@@ -1,7 +1,8 @@
 // Measurement probes for the benchmark (not part of the attention library):
 // the bf16 and FP8 (e4m3) MFMA rates this part sustains on random operands
 // with no memory or vector work, at the occupancy of the chunk attention
-// kernels (one block of eight waves per CU, two waves per SIMD).
+// kernels (one block of eight waves per CU, two waves per SIMD); and the rate
+// at which plain streaming reads of a given size come from HBM.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -70,6 +71,31 @@ int launch(const void *frags, void *out, int blocks, int iters, void *stream) {
   return (int)hipGetLastError();
 }
 
+// Streaming read: thread i of the grid reads the 16-byte words i, i + n, ...
+// (n = threads in the grid), U independent loads in flight per thread, and
+// folds them with xor; only a word that can never occur is stored, so the
+// loads cannot be dropped and nothing is written.
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+template <int U>
+__global__ __launch_bounds__(256) void read_kernel(const u32x4 *__restrict__ src, size_t n16,
+                                                   unsigned *sink) {
+  const size_t nth = (size_t)gridDim.x * 256;
+  u32x4 acc = {0, 0, 0, 0};
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += nth * U) {
+    u32x4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const size_t j = i + (size_t)u * nth;
+      v[u] = j < n16 ? src[j] : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) acc ^= v[u];
+  }
+  if ((acc[0] ^ acc[1] ^ acc[2] ^ acc[3]) == 0x9e3779b9u && acc[0] == 0x7f4a7c15u)
+    sink[blockIdx.x] = acc[1];
+}
+
 }  // namespace
 
 extern "C" {
@@ -85,6 +111,28 @@ int frt_probe_mfma_bf16(const void *frags, void *out, int blocks, int iters, voi
 
 int frt_probe_mfma_fp8(const void *frags, void *out, int blocks, int iters, void *stream) {
   return launch<i32x8>(frags, out, blocks, iters, stream);
+}
+
+// src: `bytes` of device memory (a multiple of 16), read once. sink: `blocks`
+// unsigned words (device), written only for a data pattern the caller never
+// supplies. blocks: grid size (256 threads each); unroll: loads in flight per
+// thread, 2, 4, 8 or 16. Returns 0, or hipErrorInvalidValue for bad arguments,
+// or the HIP error of the launch.
+int frt_probe_read(const void *src, size_t bytes, void *sink, int blocks, int unroll,
+                   void *stream) {
+  if (src == nullptr || sink == nullptr || bytes == 0 || bytes % 16 != 0 || blocks <= 0)
+    return (int)hipErrorInvalidValue;
+  const u32x4 *p = static_cast<const u32x4 *>(src);
+  unsigned *k = static_cast<unsigned *>(sink);
+  const hipStream_t st = (hipStream_t)stream;
+  switch (unroll) {
+    case 2: hipLaunchKernelGGL(read_kernel<2>, dim3(blocks), dim3(256), 0, st, p, bytes / 16, k); break;
+    case 4: hipLaunchKernelGGL(read_kernel<4>, dim3(blocks), dim3(256), 0, st, p, bytes / 16, k); break;
+    case 8: hipLaunchKernelGGL(read_kernel<8>, dim3(blocks), dim3(256), 0, st, p, bytes / 16, k); break;
+    case 16: hipLaunchKernelGGL(read_kernel<16>, dim3(blocks), dim3(256), 0, st, p, bytes / 16, k); break;
+    default: return (int)hipErrorInvalidValue;
+  }
+  return (int)hipGetLastError();
 }
 
 }  // extern "C"
