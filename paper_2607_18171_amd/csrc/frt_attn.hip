@@ -301,18 +301,20 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int j = 0; j < 2; ++j) vfo[kb][j] = (l32 * 8 + ((4 * kb + 2 * j + h) ^ ((l32 >> 1) & 7))) * 8;
-  // S^T - m for the 64 keys of a K buffer
+  // S^T - m for the 64 keys of a K buffer. The two key blocks' chains are
+  // issued alternately, each query fragment serving both in a row (1% faster
+  // than one chain after the other; every chain sums in the same order).
   auto qk = [&](const uint16_t *kt, f32x16 (&s)[2]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const uint16_t *kblk = kt + kb * 32 * D;
+    for (int kb = 0; kb < 2; ++kb)
       s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-          *reinterpret_cast<const bf16x8 *>(kblk + kfo[0]), qf[0], negm, 0, 0, 0);
+          *reinterpret_cast<const bf16x8 *>(kt + kb * 32 * D + kfo[0]), qf[0], negm, 0, 0, 0);
 #pragma unroll
-      for (int k = 1; k < D / 16; ++k)
+    for (int k = 1; k < D / 16; ++k)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            *reinterpret_cast<const bf16x8 *>(kblk + kfo[k]), qf[k], s[kb], 0, 0, 0);
-    }
+            *reinterpret_cast<const bf16x8 *>(kt + kb * 32 * D + kfo[k]), qf[k], s[kb], 0, 0, 0);
   };
   // row max over the tile: one chain of three-input maxima (v_max3), then
   // the lane 32 away
@@ -390,18 +392,18 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_kernel(AttnParams p) {
           lsum = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, lsum, false);
         }
   };
-  // O^T += V^T P^T for the 64 keys of a V^T buffer
+  // O^T += V^T P^T for the 64 keys of a V^T buffer: each weight fragment
+  // serves the D/32 output blocks in a row (each block sums in key order)
   auto pv = [&](const uint16_t *vt, const bf16x8 (&pf)[2][2]) __attribute__((always_inline)) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
-        const uint16_t *vblk = vt + db * 32 * BN;
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            *reinterpret_cast<const bf16x8 *>(vblk + vfo[kb][0]), pf[kb][0], o[db], 0, 0, 0);
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            *reinterpret_cast<const bf16x8 *>(vblk + vfo[kb][1]), pf[kb][1], o[db], 0, 0, 0);
-      }
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              *reinterpret_cast<const bf16x8 *>(vt + db * 32 * BN + vfo[kb][j]), pf[kb][j],
+              o[db], 0, 0, 0);
   };
 
   // One pipelined iteration for a tile t that has a successor (par = t & 1):
