@@ -61,6 +61,11 @@ SMALL = {
     "gqa_d64": shrink(WORKLOADS["prefill_swa"], B=2, Hq=6, Hkv=3, d=64, n=65, C=136,
                       rope=RopeSpec(ROPE_1D, (64, 0, 0)), mask=MaskSpec(MASK_CAUSAL, 0, 120),
                       len_lo=0, len_hi=500),
+    # G = 8 at head_dim 64 (the wide preparation blocks at the small head
+    # size), a chunk that ends 6 tokens into its second 64-token block
+    "gqa8_d64": shrink(WORKLOADS["prefill_swa"], B=2, Hq=16, Hkv=2, d=64, n=70, C=192,
+                       rope=RopeSpec(ROPE_1D, (64, 0, 0)), mask=MaskSpec(MASK_CAUSAL, 0, 150),
+                       len_lo=0, len_hi=600),
     "g8_block": shrink(WORKLOADS["prefill_swa"], B=1, Hq=16, Hkv=2, n=48, C=96,
                        mask=MaskSpec(MASK_BLOCK_CAUSAL, 48, 2), len_lo=96, len_hi=96),
     "rope_none": shrink(WORKLOADS["prefill_swa"], B=2, Hq=2, Hkv=1, n=33, C=64,
@@ -213,7 +218,7 @@ def test_deterministic_and_checkpoint_restore():
     assert torch.equal(ring.v.view(torch.int16), saved.v.view(torch.int16))
 
 
-@pytest.mark.parametrize("name", ["video_small", "video_vpart", "gqa_swa", "gqa_d64"])
+@pytest.mark.parametrize("name", ["video_small", "video_vpart", "gqa_swa", "gqa_d64", "gqa8_d64"])
 def test_stream_step_equals_attn_then_append(name):
     """frt_stream_step over consecutive steps: the same outputs and lse as
     frt_stream_attn_step + frt_kv_append, bit for bit, the same ring bytes and
