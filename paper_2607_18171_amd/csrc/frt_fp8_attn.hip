@@ -5,6 +5,15 @@
 // tile's max passes it by more than 1) so that the coded weights do not
 // depend on it: they are code(2^(s - m + 7)), the largest near 2^7.
 //
+// Raising m does not rescale O: O and the normaliser stay relative to the
+// reference max m0 of the row's first visible tile, and the PV products of
+// later tiles are scaled up by 2^(m - m0), the E8M0 scale of the MFMA's B
+// operand (one per column, i.e. per query row). Scaling by a power of two is
+// exact, so this gives the same O / sum as rescaling O at every raise, and
+// the output bits are the same; LSE takes m0. A row whose m climbs more than
+// kFrameMax above m0 re-bases (one real rescale), which keeps O far inside
+// the fp32 range.
+//
 // MFMA: v_mfma_f32_32x32x64_f8f6f4 with both operands e4m3. A lane holds 32
 // bytes of each operand: lane l is row / column l % 32, and its half
 // h = l / 32 owns 32 of the 64 k-slots. The two operands pair their slots the
@@ -217,8 +226,11 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_fp8_kernel(AttnFp8Params p
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
 #pragma unroll
   for (int r = 0; r < 16; ++r) osum[r] = 0.f;
-  float m = 0.f;  // reference max, an integer
+  float m = 0.f;   // reference max, an integer
   bool mset = false;
+  float m0 = 0.f;  // the reference max O and the normaliser are relative to
+  int bsc = 127;   // E8M0 code of 2^(m - m0): the B scale of the PV MFMAs
+  constexpr float kFrameMax = 64.f;
   const i32x8 ones8 = {0x38383838, 0x38383838, 0x38383838, 0x38383838,
                        0x38383838, 0x38383838, 0x38383838, 0x38383838};  // e4m3 1.0
 
@@ -353,24 +365,30 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_fp8_kernel(AttnFp8Params p
       }
   };
   // raise the reference max (an integer) when the tile's max exceeds it by
-  // more than kTau, or at the row's first visible key; scaling by a power of
-  // two keeps O and the normaliser exact
+  // more than kTau, or at the row's first visible key; the products of later
+  // weights carry 2^(m - m0) (see the head of the file)
   auto rescale = [&](float mraw) __attribute__((always_inline)) {
     const float mt = mraw * cq;
     const float rel = mt - m;
     const bool need = rel > kTau || (!mset && mt != kNegInf);
     if (__ballot(need)) {
       const float delta = need ? ceilf(rel) : 0.f;
-      // a row's first visible tile finds O and the sum still zero: alpha = 1
-      // there, since exp2(-delta) overflows for a tile max below -128
-      const float alpha = mset ? __builtin_amdgcn_exp2f(-delta) : 1.f;
+      const float mn = m + delta;
+      float m0n = mset ? m0 : mn;  // a row's first visible tile sets its frame
+      const bool rebase = mn - m0n > kFrameMax;
+      if (__ballot(rebase)) {
+        const float alpha = rebase ? __builtin_amdgcn_exp2f(m0n - mn) : 1.f;
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db)
+        for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) osum[r] *= alpha;
-      m += delta;
+        for (int r = 0; r < 16; ++r) osum[r] *= alpha;
+        m0n = rebase ? mn : m0n;
+      }
+      m = mn;
+      m0 = m0n;
+      bsc = 127 + (int)(m - m0);
       mset = mset || need;
     }
   };
@@ -394,9 +412,9 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_fp8_kernel(AttnFp8Params p
     for (int db = 0; db < D / 32; ++db) {
       const uint8_t *vrow = vt + db * 32 * 32 + vfo;
       o[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-          frag32(vrow, vrow + 32 * D), pf, o[db], 0, 0, 0, 0, 0, 0);
+          frag32(vrow, vrow + 32 * D), pf, o[db], 0, 0, 0, 127, 0, bsc);
     }
-    osum = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ones8, pf, osum, 0, 0, 0, 0, 0, 0);
+    osum = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ones8, pf, osum, 0, 0, 0, 127, 0, bsc);
   };
 
   auto step = [&](int t, const int par, f32x16 (&scur)[2], f32x16 (&snext)[2])
@@ -457,7 +475,7 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_fp8_kernel(AttnFp8Params p
     }
   }
 
-  // out = s_v * O / l; lse = (m - kShift + log2 l) * ln 2
+  // out = s_v * O / l (both relative to m0); lse = (m0 - kShift + log2 l) * ln 2
   const float ltot = osum[0];
   if (myrow < rows) {
     const float f = sv / ltot;
@@ -477,7 +495,7 @@ __global__ __launch_bounds__(NW * 64) void chunk_attn_fp8_kernel(AttnFp8Params p
       }
     if (p.lse != nullptr && h == 0)
       p.lse[((size_t)b * p.Hq + kvh * G + g) * n + i] =
-          (m - kShift + __builtin_amdgcn_logf(ltot)) * 0.6931471805599453f;
+          (m0 - kShift + __builtin_amdgcn_logf(ltot)) * 0.6931471805599453f;
   }
 }
 

@@ -438,3 +438,39 @@ def test_fp8_very_negative_first_tile():
                                        ks, vs)
     check_fp8(bf16_dev_to_f64(out), ref, vmax_fp8(oring, case, vs), "negative first tile")
     assert np.abs(lse.cpu().numpy() - ref_lse).max() < 2e-2
+
+
+@pytest.mark.parametrize("slope", [0.0175, 0.245])
+def test_fp8_reference_max_climbing_along_the_row(slope):
+    """Scores that rise steadily along the keys (by about 8, or about 100, base-2
+    units over a row): the reference max is raised tile after tile, the PV
+    products carry 2^(m - m0) in the MFMA's B scale, and past 64 units the row
+    re-bases once. Against the FP8 oracle within its tolerance, LSE included."""
+    wl = shrink(WORKLOADS["prefill_swa"], B=1, Hq=2, Hkv=1, n=64, C=256, rope=RopeSpec(0),
+                mask=MaskSpec(MASK_CAUSAL, 0, 0))
+    L = 160
+    case = make_case(wl, 11, lengths=np.array([L]))
+    rng = np.random.default_rng(12)
+
+    def bf16_bits(x):
+        b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+        return ((b + 0x7FFF + ((b >> 16) & 1)) >> 16).astype(np.uint16)
+
+    q = rng.standard_normal(case.q.shape).astype(np.float32) * 0.05
+    q[..., 0] = 16.0
+    case.q[:] = bf16_bits(q)
+    k0, _ = case.prior_fills[0]
+    kp = rng.standard_normal(k0.shape).astype(np.float32) * 0.05
+    kp[0, :, 0, 0] = slope * np.arange(L)
+    k0[:] = bf16_bits(kp)
+    kn = rng.standard_normal(case.k_new.shape).astype(np.float32) * 0.05
+    kn[0, :, 0, 0] = slope * np.arange(L, L + wl.n)
+    case.k_new[:] = bf16_bits(kn)
+    ks = np.full((1, 1), 0.125, np.float32)
+    vs = np.full((1, 1), 0.02, np.float32)
+    ring, oring, rope = build_fp8_rings(case, ks, vs)
+    out, lse = run_fp8_step(case, ring, rope)
+    ref, ref_lse = fp8.stream_attn_fp8(oring, case.q, case.k_new, case.v_new, wl.rope, wl.mask,
+                                       ks, vs)
+    check_fp8(bf16_dev_to_f64(out), ref, vmax_fp8(oring, case, vs), "slope %g" % slope)
+    assert np.abs(lse.cpu().numpy() - ref_lse).max() < 2e-2
