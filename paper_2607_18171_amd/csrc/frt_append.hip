@@ -102,7 +102,7 @@ __global__ __launch_bounds__(T) void chunk_prep_kernel(PrepParams p, RopeDev rop
   constexpr int CH = D / 8;
   constexpr int VS = D + 2;
   constexpr int KU = (kAppendTokens * CH + T - 1) / T;  // own-token items per thread
-  constexpr int QU = 4;                                   // query items per round
+  constexpr int QU = 4;                                   // query items per loop pass
   __shared__ uint16_t vs[kAppendTokens * VS];
   const RopeReg rg = rope_reg(rope);
   const int tb = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
